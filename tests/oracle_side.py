@@ -1,0 +1,46 @@
+"""Build the CPU oracle's view of a generated workload (tests only)."""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional
+
+import numpy as np
+
+import oracle
+from workloads import WorkloadInputs
+
+
+@dataclass
+class OracleCase:
+    layout: oracle.OracleLayout
+    store: oracle.OracleStore
+    keys: List[int]
+    pools: List[np.ndarray]
+    valid: List[np.ndarray]
+
+
+def oracle_layout(wi: WorkloadInputs) -> oracle.OracleLayout:
+    return oracle.OracleLayout.from_specs(wi.workload.chunk_tokens, wi.workload.groups)
+
+
+def build_case(wi: WorkloadInputs, held: Optional[int] = None, with_pools: bool = True,
+               tiny_payloads: bool = False) -> OracleCase:
+    """Fill an oracle store with the workload's held chunks.
+
+    ``tiny_payloads`` stores 4-byte stand-ins (enough for probe-only tests,
+    which never read payloads).
+    """
+    w = wi.workload
+    layout = oracle_layout(wi)
+    store = oracle.OracleStore(layout.n_groups)
+    keys = oracle.chain_keys(wi.tokens, w.chunk_tokens, wi.salt)
+    held = w.held_chunks if held is None else held
+    for i in range(held):
+        if tiny_payloads:
+            store.put_chunk(keys[i], [np.zeros(4, np.uint8)] * layout.n_groups)
+        else:
+            store.put_chunk(keys[i], wi.payloads(i))
+    pools = [wi.sentinel_pool(g) for g in range(layout.n_groups)] if with_pools else []
+    valid = [v.copy() for v in wi.valid_init]
+    return OracleCase(layout, store, keys, pools, valid)
