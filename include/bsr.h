@@ -1,0 +1,352 @@
+/*
+ * bsr.h -- C ABI of the Bounded-State Restoration (BSR) restore path on one
+ * MI355X (gfx950) GPU.
+ *
+ * BSR (arxiv 2608.17826) restores one rank's externally retained KV state
+ * into an engine's paged KV cache through a reusable local staging window of
+ * at most W chunks.  It has three phases (§3 "Protocol: Probe, Install,
+ * Commit"):
+ *   probe   -- find the complete reusable prefix without staging it (§3
+ *              "Probe globally"; §4 "LMCache changes", probe-only mode);
+ *   install -- move the confirmed prefix window by window through W staging
+ *              slots into the destination blocks (§2 "Bounded installation",
+ *              Eqs. 3-4; §3 "Install locally"; §4 windowed retrieve);
+ *   commit  -- expose the prefix only if every group is valid, otherwise
+ *              invalidate the whole advertised prefix (§3 Eq. 6, Prop. 2;
+ *              §4 "vLLM failure integration").
+ *
+ * Conventions
+ *   - Every function returns an int status: BSR_OK (0) or a negative
+ *     BSR_E_* code.  No exception crosses the ABI.  bsr_last_error() returns
+ *     a thread-local message describing the last failure on that thread.
+ *   - Every out-parameter is caller-allocated.  Pointers marked "device" are
+ *     HIP device pointers on the context's device; all others are host
+ *     pointers.  Streams are hipStream_t handles passed as void*.
+ *   - Sizes are in bytes unless named *_tokens, *_chunks or *_blocks.
+ *   - One context serves one GPU rank.  Store and probe calls are thread
+ *     safe; one request at a time may be bound (the bounded-retrieve lock of
+ *     §3 "Install locally"), and the calls for the bound request must come
+ *     from one thread at a time.
+ *
+ * Data layout
+ *   A chunk is chunk_tokens consecutive tokens.  A group is one allocator
+ *   group of the paged cache: n_tensors registered tensors sharing a block
+ *   size (block_tokens) and a block table.  A record is one tensor's
+ *   record_bytes for one token.
+ *   - External entry of (chunk i, group g): n_tensors * chunk_tokens records,
+ *     tensor-major then token-minor ([t][q][record]).
+ *   - Staging slot (one chunk): group g's entry at byte offset off_g, with
+ *     off_0 = 0 and off_{g+1} = off_g + align_up(payload_g, 256); the slot
+ *     size is off_G (bsr_slot_bytes).  The staging ring is W slots.
+ *   - Destination pool of tensor t of group g: pool_blocks blocks of
+ *     block_tokens * record_bytes bytes.  Token tau lives in block
+ *     block_table[tau / block_tokens] at position o = tau % block_tokens.
+ *     CONTIG blocks keep records in token order (offset o*record_bytes).
+ *     PLANAR blocks keep the first split_bytes of each record at
+ *     o*split_bytes and the remaining bytes at
+ *     block_tokens*split_bytes + o*(record_bytes - split_bytes).
+ *   - Validity: one byte per pool block per group (1 = valid state).
+ */
+#ifndef BSR_H
+#define BSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BSR_ABI_VERSION 1
+#define BSR_MAX_GROUPS 8
+#define BSR_MAX_INSTALL_BATCH 16
+#define BSR_NO_CHUNK 0xFFFFFFFFu
+
+/* status codes */
+#define BSR_OK 0
+#define BSR_E_ARG (-1)       /* invalid argument (sizes, layout, pointers, block ids) */
+#define BSR_E_STATE (-2)     /* call out of protocol order */
+#define BSR_E_MISSING (-3)   /* a store entry of the window is absent */
+#define BSR_E_CORRUPT (-4)   /* reserved for callers: corruption is reported through commit */
+#define BSR_E_TIMEOUT (-5)   /* the window's fetch exceeded its deadline */
+#define BSR_E_TRANSFER (-6)  /* a HIP transfer or launch failed */
+#define BSR_E_NOMEM (-7)     /* store arena full or host/device allocation failed */
+#define BSR_E_STAGING (-8)   /* staging buffer smaller than W * slot bytes */
+#define BSR_E_BUSY (-9)      /* another request holds the bounded-retrieve lock */
+#define BSR_E_DEVICE (-10)   /* operation needs a GPU context */
+#define BSR_E_NOTFOUND (-11) /* unknown key or request */
+
+/* failure reasons recorded in bsr_dev_status.fail */
+#define BSR_FAIL_NONE 0
+#define BSR_FAIL_MISSING 1
+#define BSR_FAIL_CORRUPT 2
+#define BSR_FAIL_TIMEOUT 3
+#define BSR_FAIL_TRANSFER 4
+#define BSR_FAIL_ABORT 5
+
+/* group kinds */
+#define BSR_KIND_CONTIG 0
+#define BSR_KIND_PLANAR 1
+
+/* bsr_config.flags */
+#define BSR_FLAG_TIME_INSTALL 1u  /* time every install launch with HIP events */
+
+/* fault injection (bsr_debug_inject), forced from the host */
+#define BSR_INJECT_NONE 0
+#define BSR_INJECT_DELAY_MS 1       /* sleep param ms before fetching chunk */
+#define BSR_INJECT_TRANSFER_ERROR 2 /* treat chunk's copy submission as failed */
+
+/* struct ids for bsr_struct_size */
+#define BSR_STRUCT_LAYOUT 1
+#define BSR_STRUCT_CONFIG 2
+#define BSR_STRUCT_GROUP_DST 3
+#define BSR_STRUCT_DEV_STATUS 4
+#define BSR_STRUCT_STATS 5
+
+typedef struct bsr_group_desc {
+  uint32_t block_tokens; /* tokens per destination block, >= 1 */
+  uint32_t n_tensors;    /* registered tensors in the group, >= 1 */
+  uint32_t record_bytes; /* bytes per token per tensor, multiple of 4 */
+  uint32_t kind;         /* BSR_KIND_CONTIG or BSR_KIND_PLANAR */
+  uint32_t split_bytes;  /* PLANAR: first-plane bytes per record, multiple of 4, < record_bytes */
+} bsr_group_desc;
+
+typedef struct bsr_layout {
+  uint32_t chunk_tokens; /* tokens per chunk (the unit of W), >= 1 */
+  uint32_t n_groups;     /* 1..BSR_MAX_GROUPS */
+  bsr_group_desc groups[BSR_MAX_GROUPS];
+} bsr_layout;
+
+typedef struct bsr_config {
+  uint32_t window_chunks;     /* W >= 1: staging slots, the restore-window size */
+  uint32_t install_batch;     /* chunks per install launch, 0 = automatic; <= min(W, BSR_MAX_INSTALL_BATCH) */
+  int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
+  uint32_t flags;             /* BSR_FLAG_* */
+  uint32_t window_timeout_ms; /* per-window fetch deadline, 0 = none */
+  uint32_t reserved[3];       /* must be 0 */
+} bsr_config;
+
+/* Destination of one group for one request (all pointers device, caller-owned). */
+typedef struct bsr_group_dst {
+  const int32_t* block_table; /* device int32[n_blocks]: physical block of the request's k-th block */
+  void* const* tensor_bases;  /* device array of n_tensors device pointers, each to a pool of
+                                 pool_blocks * block_tokens * record_bytes bytes, 16-byte aligned */
+  uint8_t* valid;             /* device uint8[pool_blocks]: validity byte per pool block */
+  uint32_t n_blocks;          /* entries in block_table; >= ceil(n_hit*chunk_tokens/block_tokens) */
+  uint32_t pool_blocks;       /* blocks per pool tensor; every block id used must be < pool_blocks */
+} bsr_group_dst;
+
+/* Request status word block, device-resident and caller-allocated (64 bytes).
+ * Written only by the library's kernels, in stream order on the compute
+ * stream.  exposed_tokens is non-zero only after a successful commit. */
+typedef struct bsr_dev_status {
+  uint32_t fail;               /* BSR_FAIL_* of the first failure, 0 = none */
+  uint32_t first_failed_chunk; /* chunk index of the first failure, BSR_NO_CHUNK = none */
+  uint32_t q[BSR_MAX_GROUPS];  /* Eq. 6 per-group validity q_g: 1 valid, 0 invalid */
+  uint64_t exposed_tokens;     /* tokens exposed as reusable (0 or n_hit*chunk_tokens) */
+  uint32_t fallback;           /* 1 when the request must fall back (failed commit or invalidate) */
+  uint32_t phase;              /* 1 bound, 2 committed, 3 invalidated */
+  uint32_t reserved[2];
+} bsr_dev_status;
+
+/* Host-side counters of the most recent (or current) bound request. */
+typedef struct bsr_stats {
+  uint64_t request_id;
+  uint32_t n_hit_chunks;        /* n: prefix length bound for restore */
+  uint32_t window_chunks;       /* W */
+  uint32_t install_batch;       /* chunks per install launch */
+  uint32_t n_windows;           /* restore_window calls accepted */
+  uint32_t n_chunks_enqueued;   /* chunks whose copy and install were enqueued */
+  uint32_t n_install_launches;
+  uint64_t slot_bytes;             /* c: bytes of one staged chunk */
+  uint64_t staging_required_bytes; /* W * slot_bytes: the ring the caller provides */
+  uint64_t peak_live_staging_bytes;/* max slots holding an unreleased chunk, times slot_bytes */
+  uint64_t aux_device_bytes;       /* library-owned device memory, O(W) (Eq. 4 M_aux) */
+  uint64_t h2d_bytes;              /* bytes enqueued host -> device */
+  uint64_t installed_bytes;        /* payload bytes enqueued for installation */
+  uint64_t exposed_tokens;         /* from the last commit */
+  int32_t fallback;                /* from the last commit or invalidate */
+  int32_t fail_reason;             /* BSR_FAIL_* from the last commit */
+  uint32_t first_failed_chunk;     /* from the last commit */
+  uint32_t q_mask;                 /* bit g = q_g from the last commit */
+  uint64_t probe_ns;               /* host time of the last probe */
+  uint64_t enqueue_ns;             /* host time spent inside restore_window calls */
+  uint64_t commit_wait_ns;         /* host time commit waited for the device */
+  double install_ms_total;         /* sum of install-kernel durations (BSR_FLAG_TIME_INSTALL) */
+  double install_ms_max;           /* longest install launch (BSR_FLAG_TIME_INSTALL) */
+} bsr_stats;
+
+typedef struct bsr_ctx bsr_ctx;
+
+/* ---- library / layout ---------------------------------------------------- */
+
+/* BSR_ABI_VERSION of the loaded library. */
+int32_t bsr_abi_version(void);
+
+/* sizeof of the public struct named by a BSR_STRUCT_* id, 0 if unknown
+ * (lets bindings check their struct mirrors). */
+uint64_t bsr_struct_size(int32_t which);
+
+/* Thread-local message of the last failure on this thread ("" if none).
+ * The pointer stays valid until the next call on this thread. */
+const char* bsr_last_error(void);
+
+/* c of §2: bytes of one staged chunk for this layout (off_G above);
+ * 0 if the layout is invalid. */
+uint64_t bsr_slot_bytes(const bsr_layout* layout);
+
+/* Eq. 5 analogue M(W) = W * c: the staging ring size the caller must
+ * provide.  0 if the layout is invalid or W == 0. */
+uint64_t bsr_staging_bytes(const bsr_layout* layout, uint32_t window_chunks);
+
+/* Chunk keys of a token sequence (§2 restore plan; the key function is this
+ * library's reading, the paper fixes none):
+ *   d_i = FNV-1a-64 of the little-endian int32 tokens of chunk i,
+ *   h_i = FNV-1a-64 of LE64(h_{i-1}) || LE64(d_i), h_{-1} = salt,
+ * for i < floor(n_tokens / chunk_tokens); a trailing partial chunk has no
+ * key.  keys_out (host, floor(n_tokens/chunk_tokens) entries) may be NULL
+ * only when there are no full chunks. */
+int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens,
+                   uint32_t chunk_tokens, uint64_t* keys_out);
+
+/* ---- context --------------------------------------------------------------- */
+
+/* Create a context for one rank.  With hip_device >= 0 the library creates
+ * its HIP events and O(W) device auxiliary state on that device; with -1 only
+ * the store and probe are usable.  *out is NULL on failure. */
+int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out);
+
+/* Destroy a context: waits for outstanding device work of a bound request,
+ * frees library-owned memory (arena, events, aux).  NULL is a no-op. */
+int bsr_ctx_destroy(bsr_ctx* ctx);
+
+/* ---- external tier: pinned-host store ---------------------------------------- */
+
+/* Reserve a library-owned pinned host arena (hipHostMalloc) of at least
+ * `bytes`, used for subsequent puts.  Needs a GPU context.  Once. */
+int bsr_store_reserve(bsr_ctx* ctx, uint64_t bytes);
+
+/* Use a caller-owned host arena of `bytes` (pinned by the caller for GPU
+ * use; plain memory is enough for host-only contexts).  The caller keeps it
+ * alive until bsr_ctx_destroy.  Once. */
+int bsr_store_adopt(bsr_ctx* ctx, void* host_arena, uint64_t bytes);
+
+/* Store one chunk under `key`: copies group_payloads[g] (payload_g bytes each,
+ * [t][q][record] order) into one arena block laid out like a staging slot,
+ * records a tag per group ((XOR of LE u32 words) << 32 | (sum of LE u32 words
+ * mod 2^32)), and publishes one entry per (key, group).  An existing entry of
+ * the key is replaced.  BSR_E_NOMEM when the arena is full. */
+int bsr_store_put_chunk(bsr_ctx* ctx, uint64_t key, const void* const* group_payloads);
+
+/* Remove the entry (key, group), or all groups of key when group < 0.  Memory
+ * in use by a bound request is freed when that request ends.
+ * BSR_E_NOTFOUND if no such entry. */
+int bsr_store_remove(bsr_ctx* ctx, uint64_t key, int32_t group);
+
+/* Host address, size and stored tag of entry (key, group).  The pointer is
+ * valid until the entry is removed or replaced; writing through it models a
+ * corrupted external object (the tag is not updated). */
+int bsr_store_payload(bsr_ctx* ctx, uint64_t key, uint32_t group, void** host_ptr,
+                      uint64_t* nbytes, uint64_t* tag);
+
+/* Number of live (key, group) entries and arena bytes in use. */
+int bsr_store_count(bsr_ctx* ctx, uint64_t* n_entries, uint64_t* bytes_used);
+
+/* ---- the hot path ------------------------------------------------------------- */
+
+/* Probe-only lookup (§3 "Probe globally", §4 probe_only).  Computes the
+ * chunk keys of `tokens` (see bsr_chunk_keys) and looks every (key, group)
+ * up in the store.  hit_bitmap bit i (LSB-first within byte i/8) is 1 iff
+ * every group of chunk i is present; *n_hit_chunks is the number of leading
+ * ones.  Nothing is staged, no reference is kept, and the store is not
+ * modified.  If the request carries a force-local marker (§3 "Recover
+ * without re-entering the same fault") the result is 0 hits and an all-zero
+ * bitmap.  The request's plan (keys, n) is kept for bsr_request_bind.
+ * hit_bitmap (ceil(N/8) bytes) and keys_out (N entries) may be NULL. */
+int bsr_probe(bsr_ctx* ctx, uint64_t request_id, uint64_t salt, const int32_t* tokens,
+              uint64_t n_tokens, uint32_t* n_hit_chunks, uint8_t* hit_bitmap,
+              uint64_t* keys_out);
+
+/* Bind a probed request for restore and take the bounded-retrieve lock
+ * (BSR_E_BUSY if another request holds it).  n_hit_chunks <= the probed n.
+ * dst: n_groups destinations (block tables are copied to the host once and
+ * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG).
+ * staging: device ring of staging_bytes >= W * slot bytes (else
+ * BSR_E_STAGING); the library uses exactly W * slot bytes of it.
+ * status: device bsr_dev_status.  Enqueues, on compute_stream, the begin
+ * kernel: status reset (fail = 0, q = 1, exposed = 0) and the valid bytes of
+ * every advertised block cleared, so no block of the prefix reads valid
+ * before commit.  copy_stream and compute_stream must be distinct. */
+int bsr_request_bind(bsr_ctx* ctx, uint64_t request_id, uint32_t n_hit_chunks,
+                     const bsr_group_dst* dst, void* staging, uint64_t staging_bytes,
+                     bsr_dev_status* status, void* copy_stream, void* compute_stream);
+
+/* Restore window [first_chunk, first_chunk + n_chunks) of the bound request
+ * (§4 windowed retrieve; 1 <= n_chunks <= W, first_chunk = the next chunk not
+ * yet requested).  Asynchronous: for each chunk it looks the entries up
+ * (a missing entry, an injected delay beyond the window deadline, or a
+ * failed copy submission fails the window), waits for the chunk's slot to be
+ * released, and enqueues the pinned-host -> slot copy on copy_stream; per
+ * install batch it enqueues the install and verify kernels on
+ * compute_stream and releases the batch's slots behind them.  On a
+ * host-detected failure it enqueues the chunks before the failing one, then
+ * an invalidate, and returns BSR_E_MISSING / BSR_E_TIMEOUT /
+ * BSR_E_TRANSFER; later windows return BSR_E_STATE.  Device-detected
+ * corruption is reported by bsr_commit. */
+int bsr_restore_window(bsr_ctx* ctx, uint64_t request_id, uint32_t first_chunk,
+                       uint32_t n_chunks);
+
+/* Report group `group` of the bound request invalid outside any transfer
+ * (its q_g of Eq. 6 becomes 0, e.g. the engine found an erroneous block in
+ * that group).  Asynchronous, on compute_stream. */
+int bsr_mark_group_invalid(bsr_ctx* ctx, uint64_t request_id, uint32_t group);
+
+/* Request-level commit (Eq. 6 with one rank).  Enqueues the commit kernel:
+ * Q = (fail == 0) and q_g for every group.  Q = 1: exposed = n*chunk_tokens
+ * and every advertised block's valid byte = 1.  Q = 0: exposed = 0, every
+ * advertised block in every group invalid, fallback = 1, and the request's
+ * force-local marker is set.  Then waits for the compute stream, reads the
+ * status back, releases store references and the bounded-retrieve lock.
+ * Returns BSR_OK in both cases; exposed_tokens / fallback (either may be
+ * NULL) report which.  All windows need not have been restored: a commit
+ * before the last window exposes nothing (the prefix is incomplete). */
+int bsr_commit(bsr_ctx* ctx, uint64_t request_id, uint64_t* exposed_tokens,
+               int32_t* fallback);
+
+/* Invalidate the bound request (§3, §4 failed-block and HMA-aware
+ * invalidation): enqueues the invalidate kernel (fail = reason if none yet,
+ * every advertised block in every group invalid, exposed = 0, fallback = 1)
+ * and sets the force-local marker.  Asynchronous and idempotent;
+ * bsr_commit or bsr_request_end completes the request.  reason: a
+ * BSR_FAIL_* value other than NONE (callers normally pass ABORT). */
+int bsr_invalidate(bsr_ctx* ctx, uint64_t request_id, int32_t reason);
+
+/* Successful RUNNING admission of a request: clears its force-local marker. */
+int bsr_request_running(bsr_ctx* ctx, uint64_t request_id);
+
+/* Request teardown: completes an uncommitted bound request (waits for its
+ * device work), releases references and the lock, clears the force-local
+ * marker and forgets the request's plan. */
+int bsr_request_end(bsr_ctx* ctx, uint64_t request_id);
+
+/* Counters of the most recent bound request. */
+int bsr_stats_get(bsr_ctx* ctx, bsr_stats* out);
+
+/* ---- instrumentation ----------------------------------------------------------- */
+
+/* Arm one host-side fault for the next restore: `kind` BSR_INJECT_* at chunk
+ * `chunk` with parameter `param`; BSR_INJECT_NONE disarms. */
+int bsr_debug_inject(bsr_ctx* ctx, int32_t kind, uint32_t chunk, uint32_t param);
+
+/* Pinned host -> device bandwidth of this context's device: best of `reps`
+ * timed hipMemcpyAsync rounds moving `bytes` from a fresh hipHostMalloc
+ * buffer to device memory, split over n_streams streams (1..4).  *gbps in
+ * 1e9 B/s.  Needs a GPU context. */
+int bsr_measure_h2d(bsr_ctx* ctx, uint64_t bytes, uint32_t n_streams, uint32_t reps,
+                    double* gbps);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BSR_H */

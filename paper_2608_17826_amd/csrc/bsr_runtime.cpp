@@ -1,0 +1,1107 @@
+// Host runtime of the bounded-window restore: external pinned-host store,
+// chunk-key chain and probe, the W-slot staging ring scheduler, and the
+// request state machine behind include/bsr.h.
+//
+// Paper map (arxiv 2608.17826):
+//   probe             §3 "Probe globally", §4 probe_only lookup
+//   window loop       §2 "Bounded installation" (Eqs. 3-4), §3 "Install
+//                     locally", §4 windowed retrieve
+//   bounded lock      §3 "Install locally" (one bounded restore at a time)
+//   commit/invalidate §3 Eq. 6 and Prop. 2, §4 "vLLM failure integration"
+//   force-local       §3 "Recover without re-entering the same fault"
+//
+// The ring: chunk i is staged in slot i mod W.  Its copy (pinned host ->
+// slot, copy stream) waits for the event that released the slot's previous
+// chunk; its install (compute stream) waits for the batch's copies.  The
+// device therefore never holds more than W staged chunks, whatever N is.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <array>
+#include <atomic>
+#include <chrono>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
+#include "bsr.h"
+#include "bsr_device.h"
+
+namespace {
+
+using bsr::FinishParams;
+using bsr::GroupGeom;
+using bsr::InstallParams;
+using bsr::TagPair;
+using bsr::VerifyParams;
+
+thread_local std::string g_err;
+
+int fail_with(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+uint64_t now_ns() {
+  return std::chrono::duration_cast<std::chrono::nanoseconds>(
+             std::chrono::steady_clock::now().time_since_epoch())
+      .count();
+}
+
+constexpr uint64_t kAlign = 256;
+constexpr uint64_t kArenaBlockAlign = 4096;
+uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// FNV-1a-64 (FNV specification: XOR the octet, multiply by the FNV prime)
+// ---------------------------------------------------------------------------
+constexpr uint64_t kFnvBasis = 0xcbf29ce484222325ull;
+constexpr uint64_t kFnvPrime = 0x00000100000001b3ull;
+
+uint64_t fnv1a64(const uint8_t* p, size_t n, uint64_t h = kFnvBasis) {
+  for (size_t i = 0; i < n; ++i) {
+    h ^= p[i];
+    h *= kFnvPrime;
+  }
+  return h;
+}
+
+bool host_is_little_endian() {
+  const uint32_t one = 1;
+  uint8_t b;
+  std::memcpy(&b, &one, 1);
+  return b == 1;
+}
+
+// d_i for every full chunk, data-parallel over chunks for long inputs.
+void chunk_digests(const int32_t* tokens, uint64_t n_chunks, uint32_t C, uint64_t* d) {
+  const uint64_t bytes = static_cast<uint64_t>(C) * 4;
+  auto work = [&](uint64_t lo, uint64_t hi) {
+    for (uint64_t i = lo; i < hi; ++i)
+      d[i] = fnv1a64(reinterpret_cast<const uint8_t*>(tokens + i * C), bytes);
+  };
+  const uint64_t total = n_chunks * bytes;
+  unsigned nt = std::thread::hardware_concurrency();
+  if (nt > 8) nt = 8;
+  if (total < (1u << 20) || nt <= 1 || n_chunks < 2 * nt) {
+    work(0, n_chunks);
+    return;
+  }
+  std::vector<std::thread> th;
+  const uint64_t per = (n_chunks + nt - 1) / nt;
+  for (unsigned t = 0; t < nt; ++t) {
+    const uint64_t lo = t * per, hi = std::min(n_chunks, lo + per);
+    if (lo < hi) th.emplace_back(work, lo, hi);
+  }
+  for (auto& x : th) x.join();
+}
+
+void chain_keys(uint64_t salt, const int32_t* tokens, uint64_t n_chunks, uint32_t C, uint64_t* keys) {
+  std::vector<uint64_t> d(n_chunks);
+  chunk_digests(tokens, n_chunks, C, d.data());
+  uint64_t h = salt;
+  for (uint64_t i = 0; i < n_chunks; ++i) {
+    uint8_t rec[16];
+    std::memcpy(rec, &h, 8);  // little-endian host (checked at entry)
+    std::memcpy(rec + 8, &d[i], 8);
+    h = fnv1a64(rec, 16);
+    keys[i] = h;
+  }
+}
+
+// (XOR of LE u32 words) << 32 | (sum mod 2^32)
+uint64_t tag_of(const uint8_t* p, uint64_t n) {
+  uint32_t s = 0, x = 0;
+  const uint64_t nw = n / 4;
+  for (uint64_t i = 0; i < nw; ++i) {
+    uint32_t w;
+    std::memcpy(&w, p + 4 * i, 4);
+    s += w;
+    x ^= w;
+  }
+  return (static_cast<uint64_t>(x) << 32) | s;
+}
+
+// ---------------------------------------------------------------------------
+// layout
+// ---------------------------------------------------------------------------
+struct Geometry {
+  bsr_layout L{};
+  uint64_t payload[BSR_MAX_GROUPS]{};
+  uint64_t offset[BSR_MAX_GROUPS]{};
+  uint64_t slot_bytes = 0;
+  uint64_t chunk_payload = 0;
+  GroupGeom gg[BSR_MAX_GROUPS]{};  // geometry without request pointers
+  uint32_t wg_start[BSR_MAX_GROUPS + 1]{};
+  uint32_t wg_per_chunk = 0;
+  uint32_t lds_bytes = 0;
+};
+
+int check_layout(const bsr_layout* L) {
+  if (!L) return fail_with(BSR_E_ARG, "layout is NULL");
+  if (L->chunk_tokens == 0) return fail_with(BSR_E_ARG, "chunk_tokens must be >= 1");
+  if (L->n_groups == 0 || L->n_groups > BSR_MAX_GROUPS)
+    return fail_with(BSR_E_ARG, "n_groups must be in 1..%d", BSR_MAX_GROUPS);
+  uint64_t slot = 0;
+  for (uint32_t g = 0; g < L->n_groups; ++g) {
+    const bsr_group_desc& d = L->groups[g];
+    if (d.block_tokens == 0 || d.n_tensors == 0) return fail_with(BSR_E_ARG, "group %u: zero block_tokens/n_tensors", g);
+    if (d.record_bytes < 4 || d.record_bytes % 4) return fail_with(BSR_E_ARG, "group %u: record_bytes must be a positive multiple of 4", g);
+    if (d.kind != BSR_KIND_CONTIG && d.kind != BSR_KIND_PLANAR) return fail_with(BSR_E_ARG, "group %u: unknown kind %u", g, d.kind);
+    if (d.kind == BSR_KIND_PLANAR && (d.split_bytes == 0 || d.split_bytes % 4 || d.split_bytes >= d.record_bytes))
+      return fail_with(BSR_E_ARG, "group %u: planar split_bytes must be a multiple of 4 in (0, record_bytes)", g);
+    if (static_cast<uint64_t>(d.block_tokens) * d.record_bytes >= (1ull << 31))
+      return fail_with(BSR_E_ARG, "group %u: block bytes too large", g);
+    slot += align_up(static_cast<uint64_t>(d.n_tensors) * L->chunk_tokens * d.record_bytes, kAlign);
+  }
+  if (slot >= (1ull << 32)) return fail_with(BSR_E_ARG, "slot bytes %llu exceed 4 GiB", (unsigned long long)slot);
+  return BSR_OK;
+}
+
+void build_geometry(const bsr_layout* L, Geometry* G) {
+  G->L = *L;
+  const uint32_t C = L->chunk_tokens;
+  uint64_t off = 0;
+  uint32_t wg = 0;
+  G->lds_bytes = 0;
+  for (uint32_t g = 0; g < L->n_groups; ++g) {
+    const bsr_group_desc& d = L->groups[g];
+    G->payload[g] = static_cast<uint64_t>(d.n_tensors) * C * d.record_bytes;
+    G->offset[g] = off;
+    off += align_up(G->payload[g], kAlign);
+    GroupGeom& q = G->gg[g];
+    q = GroupGeom{};
+    q.block_tokens = d.block_tokens;
+    q.n_tensors = d.n_tensors;
+    q.record_bytes = d.record_bytes;
+    q.kind = d.kind;
+    q.split_bytes = d.kind == BSR_KIND_PLANAR ? d.split_bytes : 0;
+    q.staged_off = static_cast<uint32_t>(G->offset[g]);
+    const uint32_t B = d.block_tokens;
+    // destination blocks one chunk can touch
+    if (C % B == 0)
+      q.segs_per_chunk = C / B;
+    else if (B % C == 0)
+      q.segs_per_chunk = 1;
+    else
+      q.segs_per_chunk = (C + B - 1) / B + 1;
+    const uint32_t seg_tokens = std::min(B, C);
+    if (d.kind == BSR_KIND_CONTIG) {
+      const uint64_t seg = static_cast<uint64_t>(seg_tokens) * d.record_bytes;
+      q.piece_bytes = bsr::kPieceBytes;
+      q.pieces_per_seg = static_cast<uint32_t>((seg + q.piece_bytes - 1) / q.piece_bytes);
+      q.piece_tokens = 0;
+    } else {
+      // tokens per LDS piece: fits the LDS budget and keeps pieces 16-byte multiples
+      uint32_t step = 16 / std::__gcd(d.record_bytes, 16u);
+      uint32_t pt = std::min(seg_tokens, bsr::kLdsCapBytes / d.record_bytes);
+      if (pt >= step) pt -= pt % step;
+      if (pt == 0) pt = 1;
+      q.piece_tokens = pt;
+      q.pieces_per_seg = (seg_tokens + pt - 1) / pt;
+      q.piece_bytes = 0;
+      const uint32_t need = static_cast<uint32_t>(align_up(static_cast<uint64_t>(pt) * d.record_bytes, 16));
+      if (need <= bsr::kLdsCapBytes) G->lds_bytes = std::max(G->lds_bytes, need);
+    }
+    G->wg_start[g] = wg;
+    wg += d.n_tensors * q.segs_per_chunk * q.pieces_per_seg;
+  }
+  G->wg_start[L->n_groups] = wg;
+  for (uint32_t g = L->n_groups + 1; g <= BSR_MAX_GROUPS; ++g) G->wg_start[g] = wg;
+  G->wg_per_chunk = wg;
+  G->slot_bytes = off;
+  G->chunk_payload = 0;
+  for (uint32_t g = 0; g < L->n_groups; ++g) G->chunk_payload += G->payload[g];
+}
+
+// ---------------------------------------------------------------------------
+// store: a pinned arena cut into slot-shaped blocks
+// ---------------------------------------------------------------------------
+struct Entry {
+  uint32_t block;
+  uint64_t tag;
+};
+
+struct BlockMeta {
+  uint32_t live_groups = 0;  // index entries pointing here
+  uint32_t refs = 0;         // references held by the bound request
+};
+
+struct Store {
+  uint8_t* arena = nullptr;
+  uint64_t arena_bytes = 0;
+  bool owned = false;
+  uint64_t block_stride = 0;
+  uint32_t n_blocks = 0;
+  std::vector<BlockMeta> meta;
+  std::vector<uint32_t> free_list;
+  uint32_t next_fresh = 0;
+  std::vector<std::unordered_map<uint64_t, Entry>> index;  // per group
+  uint64_t n_entries = 0;
+  uint32_t blocks_in_use = 0;
+
+  uint8_t* block_ptr(uint32_t b) const { return arena + static_cast<uint64_t>(b) * block_stride; }
+  bool alloc(uint32_t* b) {
+    if (!free_list.empty()) {
+      *b = free_list.back();
+      free_list.pop_back();
+    } else if (next_fresh < n_blocks) {
+      *b = next_fresh++;
+    } else {
+      return false;
+    }
+    meta[*b] = BlockMeta{};
+    ++blocks_in_use;
+    return true;
+  }
+  void maybe_free(uint32_t b) {
+    if (meta[b].live_groups == 0 && meta[b].refs == 0) {
+      free_list.push_back(b);
+      --blocks_in_use;
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// requests
+// ---------------------------------------------------------------------------
+enum class Phase { Probed, Bound, Failed, Done };
+
+struct Request {
+  std::vector<uint64_t> keys;
+  uint32_t n_probe = 0;
+  Phase phase = Phase::Probed;
+};
+
+struct Session {  // the bound request
+  uint64_t id = 0;
+  bool active = false;
+  uint32_t n_hit = 0;
+  uint32_t next_chunk = 0;
+  bool failed = false;
+  int host_fail = BSR_FAIL_NONE;
+  uint8_t* staging = nullptr;
+  bsr_dev_status* status = nullptr;
+  hipStream_t copy = nullptr, compute = nullptr;
+  InstallParams ip{};
+  FinishParams fp{};
+  std::vector<uint32_t> refs;  // arena blocks referenced
+  std::vector<int64_t> slot_free_seq;
+  int64_t copy_waited_seq = -1;
+  int64_t batch_seq = 0;
+  uint32_t slots_touched = 0;
+  std::vector<uint8_t> slot_used;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> timing;
+};
+
+struct Inject {
+  int32_t kind = BSR_INJECT_NONE;
+  uint32_t chunk = 0;
+  uint32_t param = 0;
+};
+
+}  // namespace
+
+struct bsr_ctx {
+  Geometry geo;
+  bsr_config cfg{};
+  uint32_t W = 0;
+  uint32_t batch = 0;
+  int device = -1;
+  std::mutex mu;
+  Store store;
+  std::unordered_map<uint64_t, Request> requests;
+  std::unordered_set<uint64_t> force_local;
+  Session s;
+  bsr_stats stats{};
+  Inject inject;
+  // device resources
+  TagPair* partials = nullptr;
+  uint64_t partials_bytes = 0;
+  bsr_dev_status* host_status = nullptr;  // pinned mirror
+  std::vector<hipEvent_t> full_ev, free_ev, start_ev;
+  std::vector<hipEvent_t> timing_pool;
+};
+
+namespace {
+
+int hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return BSR_OK;
+  return fail_with(BSR_E_TRANSFER, "%s: %s", what, hipGetErrorString(e));
+}
+
+int set_device(bsr_ctx* c) {
+  if (c->device < 0) return fail_with(BSR_E_DEVICE, "operation needs a GPU context (hip_device >= 0)");
+  return hip_check(hipSetDevice(c->device), "hipSetDevice");
+}
+
+hipEvent_t take_timing_event(bsr_ctx* c) {
+  if (!c->timing_pool.empty()) {
+    hipEvent_t e = c->timing_pool.back();
+    c->timing_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void release_refs(bsr_ctx* c) {
+  for (uint32_t b : c->s.refs) {
+    if (c->store.meta[b].refs) --c->store.meta[b].refs;
+    c->store.maybe_free(b);
+  }
+  c->s.refs.clear();
+}
+
+// Enqueue install + verify for the chunks staged since the last flush.
+int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags) {
+  if (chunks.empty()) return BSR_OK;
+  Session& s = c->s;
+  const uint32_t E = static_cast<uint32_t>(c->full_ev.size());
+  const int64_t seq = s.batch_seq++;
+  hipEvent_t full = c->full_ev[seq % E];
+  hipEvent_t freed = c->free_ev[seq % E];
+  int rc;
+  if ((rc = hip_check(hipEventRecord(full, s.copy), "hipEventRecord(full)"))) return rc;
+  if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
+
+  InstallParams ip = s.ip;
+  ip.n_chunks = static_cast<uint32_t>(chunks.size());
+  ip.first_chunk = chunks.front();
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
+    t0 = take_timing_event(c);
+    t1 = take_timing_event(c);
+    if (t0 && t1) (void)hipEventRecord(t0, s.compute);
+  }
+  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute), "install launch")))
+    return rc;
+  if (t0 && t1) {
+    (void)hipEventRecord(t1, s.compute);
+    s.timing.emplace_back(t0, t1);
+  }
+  VerifyParams vp{};
+  vp.partials = c->partials;
+  vp.status = s.status;
+  vp.n_chunks = ip.n_chunks;
+  vp.first_chunk = ip.first_chunk;
+  vp.n_groups = c->geo.L.n_groups;
+  vp.wg_per_chunk = ip.wg_per_chunk;
+  std::memcpy(vp.wg_start, ip.wg_start, sizeof vp.wg_start);
+  for (size_t i = 0; i < chunks.size(); ++i)
+    for (uint32_t g = 0; g < BSR_MAX_GROUPS; ++g) vp.expected[i][g] = tags[i][g];
+  if ((rc = hip_check(bsr::launch_verify(vp, s.compute), "verify launch"))) return rc;
+  if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
+  for (uint32_t ch : chunks) s.slot_free_seq[ch % c->W] = seq;
+  c->stats.n_install_launches++;
+  c->stats.installed_bytes += static_cast<uint64_t>(chunks.size()) * c->geo.chunk_payload;
+  chunks.clear();
+  tags.clear();
+  return BSR_OK;
+}
+
+int enqueue_finish(bsr_ctx* c, uint32_t mode, uint32_t reason, uint32_t chunk, uint32_t mask) {
+  FinishParams fp = c->s.fp;
+  fp.mode = mode;
+  fp.reason = reason;
+  fp.chunk = chunk;
+  fp.group_mask = mask;
+  return hip_check(bsr::launch_finish(fp, c->s.compute), "finish launch");
+}
+
+// Host-detected failure: invalidate the whole advertised prefix.
+int host_fail(bsr_ctx* c, int reason, uint32_t chunk, uint32_t mask, int code) {
+  Session& s = c->s;
+  const std::string msg = g_err;
+  int rc = enqueue_finish(c, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), chunk, mask);
+  s.failed = true;
+  if (s.host_fail == BSR_FAIL_NONE) s.host_fail = reason;
+  c->force_local.insert(s.id);
+  if (rc) return rc;
+  g_err = msg;
+  return code;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+int32_t bsr_abi_version(void) { return BSR_ABI_VERSION; }
+
+uint64_t bsr_struct_size(int32_t which) {
+  switch (which) {
+    case BSR_STRUCT_LAYOUT: return sizeof(bsr_layout);
+    case BSR_STRUCT_CONFIG: return sizeof(bsr_config);
+    case BSR_STRUCT_GROUP_DST: return sizeof(bsr_group_dst);
+    case BSR_STRUCT_DEV_STATUS: return sizeof(bsr_dev_status);
+    case BSR_STRUCT_STATS: return sizeof(bsr_stats);
+    default: return 0;
+  }
+}
+
+const char* bsr_last_error(void) { return g_err.c_str(); }
+
+uint64_t bsr_slot_bytes(const bsr_layout* layout) {
+  if (check_layout(layout)) return 0;
+  Geometry G;
+  build_geometry(layout, &G);
+  return G.slot_bytes;
+}
+
+uint64_t bsr_staging_bytes(const bsr_layout* layout, uint32_t window_chunks) {
+  if (window_chunks == 0) {
+    fail_with(BSR_E_ARG, "W must be >= 1");
+    return 0;
+  }
+  return bsr_slot_bytes(layout) * window_chunks;
+}
+
+int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens, uint32_t chunk_tokens,
+                   uint64_t* keys_out) {
+  if (!host_is_little_endian()) return fail_with(BSR_E_ARG, "big-endian host unsupported");
+  if (chunk_tokens == 0) return fail_with(BSR_E_ARG, "chunk_tokens must be >= 1");
+  const uint64_t n = n_tokens / chunk_tokens;
+  if (n == 0) return BSR_OK;
+  if (!tokens || !keys_out) return fail_with(BSR_E_ARG, "tokens/keys_out is NULL");
+  chain_keys(salt, tokens, n, chunk_tokens, keys_out);
+  return BSR_OK;
+}
+
+int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out) {
+  if (!out) return fail_with(BSR_E_ARG, "out is NULL");
+  *out = nullptr;
+  if (int rc = check_layout(layout)) return rc;
+  if (!config) return fail_with(BSR_E_ARG, "config is NULL");
+  if (config->window_chunks == 0) return fail_with(BSR_E_ARG, "W (window_chunks) must be >= 1");
+  if (config->reserved[0] || config->reserved[1] || config->reserved[2])
+    return fail_with(BSR_E_ARG, "config.reserved must be 0");
+  const uint32_t W = config->window_chunks;
+  uint32_t b = config->install_batch;
+  if (b == 0) b = std::max(1u, std::min(W / 2, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
+  if (b > W || b > BSR_MAX_INSTALL_BATCH)
+    return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
+
+  auto* c = new (std::nothrow) bsr_ctx();
+  if (!c) return fail_with(BSR_E_NOMEM, "context allocation failed");
+  build_geometry(layout, &c->geo);
+  c->cfg = *config;
+  c->W = W;
+  c->batch = b;
+  c->device = config->hip_device;
+  c->store.index.resize(layout->n_groups);
+  c->stats.window_chunks = W;
+  c->stats.install_batch = b;
+  c->stats.slot_bytes = c->geo.slot_bytes;
+  c->stats.staging_required_bytes = c->geo.slot_bytes * W;
+  if (c->device >= 0) {
+    int rc = BSR_OK;
+    int n_dev = 0;
+    if ((rc = hip_check(hipGetDeviceCount(&n_dev), "hipGetDeviceCount")) || c->device >= n_dev) {
+      delete c;
+      return rc ? rc : fail_with(BSR_E_DEVICE, "hip_device %d not present (%d devices)", config->hip_device, n_dev);
+    }
+    if ((rc = set_device(c))) {
+      delete c;
+      return rc;
+    }
+    c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * sizeof(TagPair);
+    const uint32_t E = W + 2;
+    c->full_ev.assign(E, nullptr);
+    c->free_ev.assign(E, nullptr);
+    bool ok = hipMalloc(reinterpret_cast<void**>(&c->partials), c->partials_bytes) == hipSuccess &&
+              hipHostMalloc(reinterpret_cast<void**>(&c->host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
+    for (uint32_t i = 0; ok && i < E; ++i)
+      ok = hipEventCreateWithFlags(&c->full_ev[i], hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&c->free_ev[i], hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+      bsr_ctx_destroy(c);
+      return fail_with(BSR_E_NOMEM, "device resources for W=%u could not be allocated", W);
+    }
+    c->stats.aux_device_bytes = c->partials_bytes;
+  }
+  *out = c;
+  return BSR_OK;
+}
+
+
+int bsr_ctx_destroy(bsr_ctx* c) {
+  if (!c) return BSR_OK;
+  if (c->device >= 0) {
+    (void)hipSetDevice(c->device);
+    if (c->s.active) {
+      if (c->s.copy) (void)hipStreamSynchronize(c->s.copy);
+      if (c->s.compute) (void)hipStreamSynchronize(c->s.compute);
+    }
+    for (auto e : c->full_ev)
+      if (e) (void)hipEventDestroy(e);
+    for (auto e : c->free_ev)
+      if (e) (void)hipEventDestroy(e);
+    for (auto& pr : c->s.timing) {
+      (void)hipEventDestroy(pr.first);
+      (void)hipEventDestroy(pr.second);
+    }
+    for (auto e : c->timing_pool) (void)hipEventDestroy(e);
+    if (c->partials) (void)hipFree(c->partials);
+    if (c->host_status) (void)hipHostFree(c->host_status);
+    if (c->store.owned && c->store.arena) (void)hipHostFree(c->store.arena);
+  }
+  delete c;
+  return BSR_OK;
+}
+
+// ---- store ------------------------------------------------------------------
+
+static int store_init(bsr_ctx* c, uint8_t* arena, uint64_t bytes, bool owned) {
+  Store& st = c->store;
+  st.arena = arena;
+  st.arena_bytes = bytes;
+  st.owned = owned;
+  st.block_stride = align_up(c->geo.slot_bytes, kArenaBlockAlign);
+  const uint64_t nb = bytes / st.block_stride;
+  st.n_blocks = static_cast<uint32_t>(std::min<uint64_t>(nb, 0xFFFFFFFEull));
+  st.meta.assign(st.n_blocks, BlockMeta{});
+  return BSR_OK;
+}
+
+int bsr_store_reserve(bsr_ctx* c, uint64_t bytes) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (c->store.arena) return fail_with(BSR_E_STATE, "store arena already set");
+  if (int rc = set_device(c)) return rc;
+  void* p = nullptr;
+  if (hipHostMalloc(&p, bytes ? bytes : 1, hipHostMallocDefault) != hipSuccess || !p)
+    return fail_with(BSR_E_NOMEM, "hipHostMalloc(%llu) failed", (unsigned long long)bytes);
+  return store_init(c, static_cast<uint8_t*>(p), bytes, true);
+}
+
+int bsr_store_adopt(bsr_ctx* c, void* host_arena, uint64_t bytes) {
+  if (!c || !host_arena) return fail_with(BSR_E_ARG, "ctx or arena is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (c->store.arena) return fail_with(BSR_E_STATE, "store arena already set");
+  return store_init(c, static_cast<uint8_t*>(host_arena), bytes, false);
+}
+
+static void drop_entry(bsr_ctx* c, uint32_t g, uint64_t key) {
+  auto& ix = c->store.index[g];
+  auto it = ix.find(key);
+  if (it == ix.end()) return;
+  const uint32_t b = it->second.block;
+  ix.erase(it);
+  --c->store.n_entries;
+  --c->store.meta[b].live_groups;
+  c->store.maybe_free(b);
+}
+
+int bsr_store_put_chunk(bsr_ctx* c, uint64_t key, const void* const* payloads) {
+  if (!c || !payloads) return fail_with(BSR_E_ARG, "ctx or payloads is NULL");
+  const uint32_t G = c->geo.L.n_groups;
+  for (uint32_t g = 0; g < G; ++g)
+    if (!payloads[g]) return fail_with(BSR_E_ARG, "payload of group %u is NULL", g);
+  uint32_t b;
+  uint8_t* base;
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (!c->store.arena) return fail_with(BSR_E_STATE, "no store arena (reserve or adopt first)");
+    if (!c->store.alloc(&b)) return fail_with(BSR_E_NOMEM, "store arena full (%u chunks)", c->store.n_blocks);
+    c->store.meta[b].refs = 1;  // keep the block private while it is filled
+    base = c->store.block_ptr(b);
+  }
+  uint64_t tags[BSR_MAX_GROUPS];
+  for (uint32_t g = 0; g < G; ++g) {
+    uint8_t* dst = base + c->geo.offset[g];
+    std::memcpy(dst, payloads[g], c->geo.payload[g]);
+    const uint64_t pad = align_up(c->geo.payload[g], kAlign) - c->geo.payload[g];
+    if (pad) std::memset(dst + c->geo.payload[g], 0, pad);
+    tags[g] = tag_of(dst, c->geo.payload[g]);
+  }
+  std::lock_guard<std::mutex> lk(c->mu);
+  for (uint32_t g = 0; g < G; ++g) {
+    drop_entry(c, g, key);
+    c->store.index[g][key] = Entry{b, tags[g]};
+    ++c->store.meta[b].live_groups;
+    ++c->store.n_entries;
+  }
+  c->store.meta[b].refs = 0;
+  return BSR_OK;
+}
+
+int bsr_store_remove(bsr_ctx* c, uint64_t key, int32_t group) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  const uint32_t G = c->geo.L.n_groups;
+  if (group >= static_cast<int32_t>(G)) return fail_with(BSR_E_ARG, "group %d out of range", group);
+  bool any = false;
+  for (uint32_t g = 0; g < G; ++g) {
+    if (group >= 0 && static_cast<uint32_t>(group) != g) continue;
+    if (c->store.index[g].count(key)) {
+      any = true;
+      drop_entry(c, g, key);
+    }
+  }
+  return any ? BSR_OK : fail_with(BSR_E_NOTFOUND, "no entry for key %016llx", (unsigned long long)key);
+}
+
+int bsr_store_payload(bsr_ctx* c, uint64_t key, uint32_t group, void** host_ptr, uint64_t* nbytes,
+                      uint64_t* tag) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (group >= c->geo.L.n_groups) return fail_with(BSR_E_ARG, "group %u out of range", group);
+  auto it = c->store.index[group].find(key);
+  if (it == c->store.index[group].end())
+    return fail_with(BSR_E_NOTFOUND, "no entry (%016llx, %u)", (unsigned long long)key, group);
+  if (host_ptr) *host_ptr = c->store.block_ptr(it->second.block) + c->geo.offset[group];
+  if (nbytes) *nbytes = c->geo.payload[group];
+  if (tag) *tag = it->second.tag;
+  return BSR_OK;
+}
+
+int bsr_store_count(bsr_ctx* c, uint64_t* n_entries, uint64_t* bytes_used) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (n_entries) *n_entries = c->store.n_entries;
+  if (bytes_used) *bytes_used = static_cast<uint64_t>(c->store.blocks_in_use) * c->store.block_stride;
+  return BSR_OK;
+}
+
+// ---- probe --------------------------------------------------------------------
+
+int bsr_probe(bsr_ctx* c, uint64_t request_id, uint64_t salt, const int32_t* tokens, uint64_t n_tokens,
+              uint32_t* n_hit_chunks, uint8_t* hit_bitmap, uint64_t* keys_out) {
+  if (!c || !n_hit_chunks) return fail_with(BSR_E_ARG, "ctx or n_hit_chunks is NULL");
+  if (!host_is_little_endian()) return fail_with(BSR_E_ARG, "big-endian host unsupported");
+  const uint64_t t0 = now_ns();
+  const uint32_t C = c->geo.L.chunk_tokens;
+  const uint64_t N = n_tokens / C;
+  if (N > 0xFFFFFFF0ull) return fail_with(BSR_E_ARG, "too many chunks");
+  if (N && !tokens) return fail_with(BSR_E_ARG, "tokens is NULL");
+  Request req;
+  req.keys.resize(N);
+  if (N) chain_keys(salt, tokens, N, C, req.keys.data());
+  if (hit_bitmap) std::memset(hit_bitmap, 0, (N + 7) / 8);
+  uint32_t n_hit = 0;
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (c->s.active && c->s.id == request_id)
+      return fail_with(BSR_E_STATE, "request %llu is bound; end it before probing again", (unsigned long long)request_id);
+    const bool local = c->force_local.count(request_id) != 0;
+    bool prefix = true;
+    const uint32_t G = c->geo.L.n_groups;
+    for (uint64_t i = 0; i < N && !local; ++i) {
+      bool hit = true;
+      for (uint32_t g = 0; g < G && hit; ++g) hit = c->store.index[g].count(req.keys[i]) != 0;
+      if (hit && hit_bitmap) hit_bitmap[i >> 3] |= static_cast<uint8_t>(1u << (i & 7));
+      if (!hit) prefix = false;
+      if (prefix) ++n_hit;
+    }
+    req.n_probe = n_hit;
+    if (keys_out && N) std::memcpy(keys_out, req.keys.data(), N * 8);
+    c->requests[request_id] = std::move(req);
+    c->stats.probe_ns = now_ns() - t0;
+  }
+  *n_hit_chunks = n_hit;
+  return BSR_OK;
+}
+
+// ---- bind ----------------------------------------------------------------------
+
+int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_group_dst* dst,
+                     void* staging, uint64_t staging_bytes, bsr_dev_status* status, void* copy_stream,
+                     void* compute_stream) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (int rc = set_device(c)) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (c->s.active)
+    return fail_with(BSR_E_BUSY, "request %llu holds the bounded-retrieve lock", (unsigned long long)c->s.id);
+  auto it = c->requests.find(request_id);
+  if (it == c->requests.end()) return fail_with(BSR_E_STATE, "request %llu was not probed", (unsigned long long)request_id);
+  Request& rq = it->second;
+  if (rq.phase != Phase::Probed) return fail_with(BSR_E_STATE, "request %llu already bound once; probe again", (unsigned long long)request_id);
+  if (n_hit > rq.n_probe) return fail_with(BSR_E_ARG, "n_hit_chunks %u exceeds the probed prefix %u", n_hit, rq.n_probe);
+  if (!dst || !staging || !status) return fail_with(BSR_E_ARG, "dst, staging or status is NULL");
+  if (!copy_stream || !compute_stream || copy_stream == compute_stream)
+    return fail_with(BSR_E_ARG, "copy and compute streams must be distinct non-null streams");
+  const uint64_t need = c->geo.slot_bytes * c->W;
+  if (staging_bytes < need)
+    return fail_with(BSR_E_STAGING, "staging %llu B < W x slot = %llu B", (unsigned long long)staging_bytes, (unsigned long long)need);
+  if (reinterpret_cast<uintptr_t>(staging) % 256) return fail_with(BSR_E_ARG, "staging must be 256-byte aligned");
+
+  const uint32_t G = c->geo.L.n_groups, C = c->geo.L.chunk_tokens;
+  hipStream_t compute = static_cast<hipStream_t>(compute_stream);
+  FinishParams fp{};
+  fp.status = status;
+  fp.n_groups = G;
+  fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
+  InstallParams ip{};
+  ip.ring = static_cast<const uint8_t*>(staging);
+  ip.slot_bytes = c->geo.slot_bytes;
+  ip.window = c->W;
+  ip.chunk_tokens = C;
+  ip.n_groups = G;
+  ip.wg_per_chunk = c->geo.wg_per_chunk;
+  std::memcpy(ip.wg_start, c->geo.wg_start, sizeof ip.wg_start);
+  ip.lds_bytes = c->geo.lds_bytes;
+  ip.partials = c->partials;
+  ip.status = status;
+  uint32_t total = 0;
+  std::vector<int32_t> bt;
+  for (uint32_t g = 0; g < G; ++g) {
+    const bsr_group_dst& d = dst[g];
+    const uint32_t B = c->geo.L.groups[g].block_tokens;
+    const uint64_t nreq = (static_cast<uint64_t>(n_hit) * C + B - 1) / B;
+    if (!d.block_table || !d.tensor_bases || !d.valid) return fail_with(BSR_E_ARG, "group %u: NULL destination pointer", g);
+    if (d.n_blocks < nreq) return fail_with(BSR_E_ARG, "group %u: block table has %u blocks, prefix needs %llu", g, d.n_blocks, (unsigned long long)nreq);
+    if (d.pool_blocks == 0) return fail_with(BSR_E_ARG, "group %u: pool_blocks is 0", g);
+    // copy the advertised part of the block table back once and check it
+    bt.resize(nreq);
+    if (nreq) {
+      int rc = hip_check(hipMemcpyAsync(bt.data(), d.block_table, nreq * 4, hipMemcpyDeviceToHost, compute), "block table readback");
+      if (!rc) rc = hip_check(hipStreamSynchronize(compute), "hipStreamSynchronize");
+      if (rc) return rc;
+    }
+    std::vector<uint8_t> seen(d.pool_blocks, 0);
+    for (uint64_t k = 0; k < nreq; ++k) {
+      const int32_t b = bt[k];
+      if (b < 0 || static_cast<uint32_t>(b) >= d.pool_blocks)
+        return fail_with(BSR_E_ARG, "group %u: block_table[%llu] = %d outside [0, %u)", g, (unsigned long long)k, b, d.pool_blocks);
+      if (seen[b]++) return fail_with(BSR_E_ARG, "group %u: block %d appears twice in the prefix", g, b);
+    }
+    GroupGeom q = c->geo.gg[g];
+    q.pool_blocks = d.pool_blocks;
+    q.n_blocks = d.n_blocks;
+    q.block_table = d.block_table;
+    q.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
+    ip.g[g] = q;
+    fp.g[g] = bsr::GroupValid{d.block_table, d.valid, static_cast<uint32_t>(nreq), d.pool_blocks};
+    total += static_cast<uint32_t>(nreq);
+  }
+  fp.total_blocks = total;
+
+  Session& s = c->s;
+  s = Session{};
+  s.id = request_id;
+  s.n_hit = n_hit;
+  s.staging = static_cast<uint8_t*>(staging);
+  s.status = status;
+  s.copy = static_cast<hipStream_t>(copy_stream);
+  s.compute = compute;
+  s.ip = ip;
+  s.fp = fp;
+  s.slot_free_seq.assign(c->W, -1);
+  s.slot_used.assign(c->W, 0);
+
+  // begin: reset the status words and clear the advertised valid bytes
+  FinishParams begin = fp;
+  begin.mode = bsr::kFinishBegin;
+  if (int rc = hip_check(bsr::launch_finish(begin, compute), "begin launch")) return rc;
+  // no copy of this request may overwrite the ring before earlier compute work is done
+  if (int rc = hip_check(hipEventRecord(c->free_ev[0], compute), "hipEventRecord")) return rc;
+  if (int rc = hip_check(hipStreamWaitEvent(s.copy, c->free_ev[0], 0), "hipStreamWaitEvent")) return rc;
+  s.batch_seq = 1;  // event slot 0 is used by the bind fence above
+  s.active = true;
+  rq.phase = Phase::Bound;
+
+  bsr_stats& st = c->stats;
+  const uint64_t aux = st.aux_device_bytes;
+  st = bsr_stats{};
+  st.request_id = request_id;
+  st.n_hit_chunks = n_hit;
+  st.window_chunks = c->W;
+  st.install_batch = c->batch;
+  st.slot_bytes = c->geo.slot_bytes;
+  st.staging_required_bytes = need;
+  st.aux_device_bytes = aux;
+  st.first_failed_chunk = BSR_NO_CHUNK;
+  return BSR_OK;
+}
+
+// ---- restore window ------------------------------------------------------------
+
+int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, uint32_t n_chunks) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (int rc = set_device(c)) return rc;
+  const uint64_t t_enter = now_ns();
+  std::lock_guard<std::mutex> lk(c->mu);
+  Session& s = c->s;
+  if (!s.active || s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  if (s.failed) return fail_with(BSR_E_STATE, "request %llu already failed", (unsigned long long)request_id);
+  if (n_chunks == 0 || n_chunks > c->W) return fail_with(BSR_E_ARG, "n_chunks %u must be in 1..W=%u", n_chunks, c->W);
+  if (first_chunk != s.next_chunk) return fail_with(BSR_E_STATE, "window starts at %u, expected %u", first_chunk, s.next_chunk);
+  if (static_cast<uint64_t>(first_chunk) + n_chunks > s.n_hit)
+    return fail_with(BSR_E_ARG, "window [%u, %u) beyond the bound prefix %u", first_chunk, first_chunk + n_chunks, s.n_hit);
+
+  const Request& rq = c->requests[request_id];
+  const uint32_t G = c->geo.L.n_groups;
+  const uint32_t all_mask = (G >= 32) ? 0xFFFFFFFFu : ((1u << G) - 1);
+  const uint32_t E = static_cast<uint32_t>(c->free_ev.size());
+  std::vector<uint32_t> batch;
+  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>> tags;
+  batch.reserve(c->batch);
+  tags.reserve(c->batch);
+  const uint64_t t_window = now_ns();
+  int rc = BSR_OK;
+
+  for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {
+    // injected host faults (forced from the host; kernels always exit normally)
+    if (c->inject.kind == BSR_INJECT_DELAY_MS && c->inject.chunk == i)
+      std::this_thread::sleep_for(std::chrono::milliseconds(c->inject.param));
+    if (c->cfg.window_timeout_ms &&
+        (now_ns() - t_window) > static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull) {
+      if ((rc = flush_batch(c, batch, tags))) return rc;
+      fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded at chunk %u", c->cfg.window_timeout_ms, i);
+      return host_fail(c, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
+    }
+    if (c->inject.kind == BSR_INJECT_TRANSFER_ERROR && c->inject.chunk == i) {
+      if ((rc = flush_batch(c, batch, tags))) return rc;
+      fail_with(BSR_E_TRANSFER, "injected transfer error at chunk %u", i);
+      return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+    }
+    // fetch: every group's entry must be present
+    const uint64_t key = rq.keys[i];
+    uint32_t missing = 0;
+    Entry ent[BSR_MAX_GROUPS];
+    for (uint32_t g = 0; g < G; ++g) {
+      auto it = c->store.index[g].find(key);
+      if (it == c->store.index[g].end())
+        missing |= 1u << g;
+      else
+        ent[g] = it->second;
+    }
+    if (missing) {
+      if ((rc = flush_batch(c, batch, tags))) return rc;
+      fail_with(BSR_E_MISSING, "chunk %u: entries missing for group mask 0x%x", i, missing);
+      return host_fail(c, BSR_FAIL_MISSING, i, missing, BSR_E_MISSING);
+    }
+    bool one_block = true;
+    for (uint32_t g = 1; g < G; ++g) one_block = one_block && ent[g].block == ent[0].block;
+    for (uint32_t g = 0; g < G; ++g) {
+      if (g == 0 || !one_block) {
+        ++c->store.meta[ent[g].block].refs;
+        s.refs.push_back(ent[g].block);
+      }
+    }
+    // the slot must have been released by the install of its previous chunk
+    const uint32_t slot = i % c->W;
+    const int64_t need_seq = s.slot_free_seq[slot];
+    if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
+      if ((rc = hip_check(hipStreamWaitEvent(s.copy, c->free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
+      s.copy_waited_seq = need_seq;
+    }
+    uint8_t* dst = s.staging + static_cast<uint64_t>(slot) * c->geo.slot_bytes;
+    hipError_t e = hipSuccess;
+    if (one_block) {
+      e = hipMemcpyAsync(dst, c->store.block_ptr(ent[0].block), c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
+    } else {
+      for (uint32_t g = 0; g < G && e == hipSuccess; ++g)
+        e = hipMemcpyAsync(dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
+                           c->geo.payload[g], hipMemcpyHostToDevice, s.copy);
+    }
+    if (e != hipSuccess) {
+      const std::string why = hipGetErrorString(e);
+      if ((rc = flush_batch(c, batch, tags))) return rc;
+      fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
+      return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+    }
+    c->stats.h2d_bytes += c->geo.slot_bytes;
+    if (!s.slot_used[slot]) {
+      s.slot_used[slot] = 1;
+      ++s.slots_touched;
+    }
+    std::array<uint64_t, BSR_MAX_GROUPS> tg{};
+    for (uint32_t g = 0; g < G; ++g) tg[g] = ent[g].tag;
+    batch.push_back(i);
+    tags.push_back(tg);
+    ++c->stats.n_chunks_enqueued;
+    if (batch.size() == c->batch)
+      if ((rc = flush_batch(c, batch, tags))) return rc;
+  }
+  if ((rc = flush_batch(c, batch, tags))) return rc;
+  s.next_chunk = first_chunk + n_chunks;
+  ++c->stats.n_windows;
+  c->stats.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
+  c->stats.enqueue_ns += now_ns() - t_enter;
+  return BSR_OK;
+}
+
+int bsr_mark_group_invalid(bsr_ctx* c, uint64_t request_id, uint32_t group) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (int rc = set_device(c)) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  if (group >= c->geo.L.n_groups) return fail_with(BSR_E_ARG, "group %u out of range", group);
+  return enqueue_finish(c, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group);
+}
+
+int bsr_invalidate(bsr_ctx* c, uint64_t request_id, int32_t reason) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (int rc = set_device(c)) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  if (reason <= BSR_FAIL_NONE || reason > BSR_FAIL_ABORT) return fail_with(BSR_E_ARG, "invalid reason %d", reason);
+  c->force_local.insert(request_id);
+  c->s.failed = true;
+  if (c->s.host_fail == BSR_FAIL_NONE) c->s.host_fail = reason;
+  return enqueue_finish(c, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), BSR_NO_CHUNK, 0);
+}
+
+// Wait for the bound request's device work, read its status, release it.
+static int complete_session(bsr_ctx* c, bool run_commit, uint64_t* exposed, int32_t* fallback) {
+  Session& s = c->s;
+  int rc = BSR_OK;
+  if (run_commit) {
+    if (!s.failed && s.next_chunk < s.n_hit) {
+      // an incomplete prefix is never exposed
+      rc = enqueue_finish(c, bsr::kFinishInvalidate, BSR_FAIL_ABORT, BSR_NO_CHUNK, 0);
+      s.failed = true;
+    }
+    if (!rc) rc = enqueue_finish(c, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
+  }
+  const uint64_t t0 = now_ns();
+  if (!rc) rc = hip_check(hipMemcpyAsync(c->host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
+  int rc2 = hip_check(hipStreamSynchronize(s.compute), "hipStreamSynchronize(compute)");
+  int rc3 = hip_check(hipStreamSynchronize(s.copy), "hipStreamSynchronize(copy)");
+  if (!rc) rc = rc2 ? rc2 : rc3;
+  c->stats.commit_wait_ns = now_ns() - t0;
+  if (!rc) {
+    const bsr_dev_status& h = *c->host_status;
+    c->stats.exposed_tokens = h.exposed_tokens;
+    c->stats.fallback = static_cast<int32_t>(h.fallback);
+    c->stats.fail_reason = static_cast<int32_t>(h.fail);
+    c->stats.first_failed_chunk = h.first_failed_chunk;
+    uint32_t m = 0;
+    for (uint32_t g = 0; g < c->geo.L.n_groups; ++g)
+      if (h.q[g]) m |= 1u << g;
+    c->stats.q_mask = m;
+    if (h.fallback) c->force_local.insert(s.id);
+    if (exposed) *exposed = h.exposed_tokens;
+    if (fallback) *fallback = static_cast<int32_t>(h.fallback);
+  } else {
+    c->force_local.insert(s.id);
+    if (exposed) *exposed = 0;
+    if (fallback) *fallback = 1;
+  }
+  double tot = 0, mx = 0;
+  for (auto& pr : s.timing) {
+    float ms = 0;
+    if (hipEventElapsedTime(&ms, pr.first, pr.second) == hipSuccess) {
+      tot += ms;
+      mx = std::max(mx, static_cast<double>(ms));
+    }
+    c->timing_pool.push_back(pr.first);
+    c->timing_pool.push_back(pr.second);
+  }
+  s.timing.clear();
+  c->stats.install_ms_total = tot;
+  c->stats.install_ms_max = mx;
+  release_refs(c);
+  auto it = c->requests.find(s.id);
+  if (it != c->requests.end()) it->second.phase = Phase::Done;
+  s.active = false;
+  c->inject = Inject{};
+  return rc;
+}
+
+int bsr_commit(bsr_ctx* c, uint64_t request_id, uint64_t* exposed_tokens, int32_t* fallback) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (int rc = set_device(c)) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  return complete_session(c, true, exposed_tokens, fallback);
+}
+
+int bsr_request_running(bsr_ctx* c, uint64_t request_id) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  c->force_local.erase(request_id);
+  return BSR_OK;
+}
+
+int bsr_request_end(bsr_ctx* c, uint64_t request_id) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  int rc = BSR_OK;
+  if (c->s.active && c->s.id == request_id) {
+    if ((rc = set_device(c))) return rc;
+    rc = complete_session(c, false, nullptr, nullptr);
+  }
+  c->force_local.erase(request_id);
+  c->requests.erase(request_id);
+  return rc;
+}
+
+int bsr_stats_get(bsr_ctx* c, bsr_stats* out) {
+  if (!c || !out) return fail_with(BSR_E_ARG, "ctx or out is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  *out = c->stats;
+  return BSR_OK;
+}
+
+int bsr_debug_inject(bsr_ctx* c, int32_t kind, uint32_t chunk, uint32_t param) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (kind < BSR_INJECT_NONE || kind > BSR_INJECT_TRANSFER_ERROR) return fail_with(BSR_E_ARG, "unknown inject kind %d", kind);
+  std::lock_guard<std::mutex> lk(c->mu);
+  c->inject = Inject{kind, chunk, param};
+  return BSR_OK;
+}
+
+int bsr_measure_h2d(bsr_ctx* c, uint64_t bytes, uint32_t n_streams, uint32_t reps, double* gbps) {
+  if (!c || !gbps || bytes == 0 || reps == 0) return fail_with(BSR_E_ARG, "bad arguments");
+  if (n_streams < 1 || n_streams > 4) return fail_with(BSR_E_ARG, "n_streams must be 1..4");
+  if (int rc = set_device(c)) return rc;
+  void* h = nullptr;
+  void* d = nullptr;
+  hipStream_t st[4] = {};
+  hipEvent_t ev[6] = {};
+  int rc = BSR_OK;
+  if (hipHostMalloc(&h, bytes, hipHostMallocDefault) != hipSuccess || hipMalloc(&d, bytes) != hipSuccess)
+    rc = fail_with(BSR_E_NOMEM, "buffers for the H2D measurement");
+  for (uint32_t i = 0; !rc && i < n_streams; ++i) rc = hip_check(hipStreamCreate(&st[i]), "hipStreamCreate");
+  for (int i = 0; !rc && i < 6; ++i) rc = hip_check(hipEventCreate(&ev[i]), "hipEventCreate");
+  if (!rc) {
+    std::memset(h, 0x5a, bytes);
+    double best = 0;
+    const uint64_t part = (bytes / n_streams) & ~uint64_t(4095);
+    for (uint32_t r = 0; r < reps && !rc; ++r) {
+      rc = hip_check(hipEventRecord(ev[0], st[0]), "hipEventRecord");
+      for (uint32_t i = 1; !rc && i < n_streams; ++i) rc = hip_check(hipStreamWaitEvent(st[i], ev[0], 0), "wait");
+      for (uint32_t i = 0; !rc && i < n_streams; ++i) {
+        const uint64_t off = part * i;
+        const uint64_t len = (i + 1 == n_streams) ? bytes - off : part;
+        rc = hip_check(hipMemcpyAsync(static_cast<uint8_t*>(d) + off, static_cast<uint8_t*>(h) + off, len, hipMemcpyHostToDevice, st[i]), "hipMemcpyAsync");
+        if (!rc && i) rc = hip_check(hipEventRecord(ev[1 + i], st[i]), "hipEventRecord");
+        if (!rc && i) rc = hip_check(hipStreamWaitEvent(st[0], ev[1 + i], 0), "wait");
+      }
+      if (!rc) rc = hip_check(hipEventRecord(ev[5], st[0]), "hipEventRecord");
+      if (!rc) rc = hip_check(hipEventSynchronize(ev[5]), "hipEventSynchronize");
+      float ms = 0;
+      if (!rc) rc = hip_check(hipEventElapsedTime(&ms, ev[0], ev[5]), "hipEventElapsedTime");
+      if (!rc && ms > 0) best = std::max(best, bytes / (ms * 1e-3) / 1e9);
+    }
+    *gbps = best;
+  }
+  for (uint32_t i = 0; i < n_streams; ++i)
+    if (st[i]) (void)hipStreamSynchronize(st[i]);
+  for (auto e : ev)
+    if (e) (void)hipEventDestroy(e);
+  for (auto s2 : st)
+    if (s2) (void)hipStreamDestroy(s2);
+  if (d) (void)hipFree(d);
+  if (h) (void)hipHostFree(h);
+  return rc;
+}
+
+}  // extern "C"

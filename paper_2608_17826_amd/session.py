@@ -1,0 +1,80 @@
+"""Restore-session helper over the C ABI, with torch as the memory plumbing.
+
+Allocates the W-slot staging ring (exactly ``bsr_staging_bytes`` bytes) and
+the device status block with torch, creates two default-priority streams
+(copy, compute), and drives one request through bind -> restore_window x K
+-> commit.  All restore work runs inside libbsr.so.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import bsr
+
+
+@dataclass
+class Outcome:
+    exposed_tokens: int
+    fallback: int
+    window_errors: List[Tuple[int, int]] = field(default_factory=list)  # (first_chunk, code)
+    stats: dict = field(default_factory=dict)
+    status: dict = field(default_factory=dict)
+
+
+def group_dsts(block_tables: Sequence[torch.Tensor], tensor_bases: Sequence[torch.Tensor],
+               valid: Sequence[torch.Tensor], pool_blocks: Sequence[int]) -> List[bsr.bsr_group_dst]:
+    return [bsr.group_dst(bt.data_ptr(), tb.data_ptr(), v.data_ptr(), bt.numel(), pb)
+            for bt, tb, v, pb in zip(block_tables, tensor_bases, valid, pool_blocks)]
+
+
+def status_dict(raw: torch.Tensor) -> dict:
+    h = raw.cpu().numpy()
+    s = bsr.bsr_dev_status.from_buffer_copy(h.tobytes())
+    return {"fail": s.fail, "first_failed_chunk": s.first_failed_chunk, "q": list(s.q),
+            "exposed_tokens": s.exposed_tokens, "fallback": s.fallback, "phase": s.phase}
+
+
+class RestoreSession:
+    def __init__(self, ctx: bsr.Ctx, device: str = "cuda:0"):
+        self.ctx = ctx
+        self.device = torch.device(device)
+        self.staging_bytes = bsr.bsr_staging_bytes(ctx.layout, ctx.window_chunks)
+        self.staging = torch.empty(self.staging_bytes, dtype=torch.uint8, device=self.device)
+        self.status = torch.zeros(64, dtype=torch.uint8, device=self.device)
+        self.copy_stream = torch.cuda.Stream(device=self.device)
+        self.compute_stream = torch.cuda.Stream(device=self.device)
+
+    def bind(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst]) -> None:
+        bsr.bsr_request_bind(self.ctx, request_id, n_hit, dsts, self.staging.data_ptr(),
+                             self.staging_bytes, self.status.data_ptr(),
+                             self.copy_stream.cuda_stream, self.compute_stream.cuda_stream)
+
+    def windows(self, n_hit: int) -> List[Tuple[int, int]]:
+        W = self.ctx.window_chunks
+        return [(s, min(W, n_hit - s)) for s in range(0, n_hit, W)]
+
+    def restore(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst],
+                plan: Optional[Sequence[Tuple[int, int]]] = None, abort_after_windows: Optional[int] = None,
+                before_commit=None) -> Outcome:
+        """bind, every window of the plan, then commit (or invalidate + commit)."""
+        torch.cuda.current_stream(self.device).synchronize()  # inputs written by torch are ready
+        self.bind(request_id, n_hit, dsts)
+        errors = []
+        for j, (first, n) in enumerate(plan if plan is not None else self.windows(n_hit)):
+            try:
+                bsr.bsr_restore_window(self.ctx, request_id, first, n)
+            except bsr.BsrError as e:
+                errors.append((first, e.code))
+                break
+            if abort_after_windows is not None and j + 1 >= abort_after_windows:
+                bsr.bsr_invalidate(self.ctx, request_id, bsr.BSR_FAIL_ABORT)
+                break
+        if before_commit is not None:
+            before_commit()
+        exposed, fallback = bsr.bsr_commit(self.ctx, request_id)
+        return Outcome(exposed, fallback, errors, bsr.bsr_stats_get(self.ctx), status_dict(self.status))

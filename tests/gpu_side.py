@@ -1,0 +1,85 @@
+"""Drive the HIP path on a generated workload (GPU tests only)."""
+
+from __future__ import annotations
+
+import sys
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+from paper_2608_17826_amd import bsr
+from paper_2608_17826_amd.session import RestoreSession, group_dsts
+from workloads import WorkloadInputs
+from workloads.device import place
+
+KIND = {"contig": bsr.BSR_KIND_CONTIG, "planar": bsr.BSR_KIND_PLANAR}
+
+
+def layout_of(wi: WorkloadInputs) -> bsr.bsr_layout:
+    w = wi.workload
+    return bsr.make_layout(w.chunk_tokens, [(s.block_tokens, s.n_tensors, s.record_bytes, KIND[s.kind],
+                                             s.split_bytes) for s in w.groups])
+
+
+def say(*a) -> None:
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+class GpuCase:
+    """Library context + pinned store holding the workload's chunks + device pools."""
+
+    def __init__(self, wi: WorkloadInputs, W: int, install_batch: int = 0, flags: int = 0,
+                 timeout_ms: int = 0, held: Optional[int] = None, device: str = "cuda:0"):
+        self.wi = wi
+        w = wi.workload
+        self.layout = layout_of(wi)
+        self.ctx = bsr.bsr_ctx_create(self.layout, W, hip_device=0, install_batch=install_batch,
+                                      flags=flags, window_timeout_ms=timeout_ms)
+        held = w.held_chunks if held is None else held
+        slot = bsr.bsr_slot_bytes(self.layout)
+        stride = (slot + 4095) // 4096 * 4096
+        bsr.bsr_store_reserve(self.ctx, stride * (held + 2))
+        self.keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
+        self._put(held)
+        self.dev = place(wi, device)
+        torch.cuda.synchronize()
+        self.session = RestoreSession(self.ctx, device)
+
+    def _put(self, held: int) -> None:
+        def put(i):
+            bsr.bsr_store_put_chunk(self.ctx, int(self.keys[i]), self.wi.payloads(i))
+        if held > 64:
+            with ThreadPoolExecutor(8) as ex:
+                list(ex.map(put, range(held)))
+        else:
+            for i in range(held):
+                put(i)
+
+    def dsts(self):
+        return group_dsts(self.dev.block_tables, self.dev.tensor_bases, self.dev.valid, self.wi.pool_blocks)
+
+    def probe(self, request_id: int, salt: Optional[int] = None):
+        return bsr.bsr_probe(self.ctx, request_id, self.wi.salt if salt is None else salt, self.wi.tokens)
+
+    def restore(self, request_id: int, n_hit: int, **kw):
+        return self.session.restore(request_id, n_hit, self.dsts(), **kw)
+
+    def pool_host(self, g: int) -> np.ndarray:
+        return np.stack([p.cpu().numpy() for p in self.dev.pools[g]])
+
+    def valid_host(self, g: int) -> np.ndarray:
+        return self.dev.valid[g].cpu().numpy()
+
+    def corrupt(self, key: int, g: int, byte: int, mask: int) -> None:
+        import ctypes
+        addr, n, _ = bsr.bsr_store_payload(self.ctx, key, g)
+        assert 0 <= byte < n
+        b = ctypes.c_uint8.from_address(addr + byte)
+        b.value ^= mask
+
+    def close(self) -> None:
+        bsr.bsr_ctx_destroy(self.ctx)

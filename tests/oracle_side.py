@@ -44,3 +44,34 @@ def build_case(wi: WorkloadInputs, held: Optional[int] = None, with_pools: bool 
     pools = [wi.sentinel_pool(g) for g in range(layout.n_groups)] if with_pools else []
     valid = [v.copy() for v in wi.valid_init]
     return OracleCase(layout, store, keys, pools, valid)
+
+
+class GeneratorStore:
+    """Read-only stand-in for OracleStore over a workload's generated payloads.
+
+    Presents the entries of chunks [0, held) under the oracle's chunk keys,
+    minus removed ones, with tags computed by the oracle on first use; lets
+    full-size checks call the oracle without copying the whole external tier.
+    """
+
+    def __init__(self, wi: WorkloadInputs, keys: List[int], held: Optional[int] = None):
+        self.wi = wi
+        self.n_groups = len(wi.workload.groups)
+        held = wi.workload.held_chunks if held is None else held
+        self.index = {int(k): i for i, k in enumerate(keys[:held])}
+        self.removed = set()
+        self._tags = {}
+
+    def has(self, key: int, g: int) -> bool:
+        return int(key) in self.index and (int(key), g) not in self.removed
+
+    def get(self, key: int, g: int):
+        i = self.index[int(key)]
+        p = self.wi.payload(i, g)
+        if (i, g) not in self._tags:
+            self._tags[(i, g)] = oracle.entry_tag(p)
+        return p, self._tags[(i, g)]
+
+    def remove(self, key: int, g: int = -1) -> None:
+        for gg in (range(self.n_groups) if g < 0 else [g]):
+            self.removed.add((int(key), gg))

@@ -1,0 +1,215 @@
+"""Parity of the HIP path with the CPU oracle (GPU).
+
+Small cases compare every destination byte, every valid byte, the status
+words and the byte counters.  Failure cases compare what the commit rule
+fixes: exposure, fallback, every valid byte, every block outside the
+advertised prefix, the first failed chunk and the reason (request blocks
+themselves are unspecified after a failure: they are never exposed).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_side import GpuCase, say
+from oracle_side import build_case
+from paper_2608_17826_amd import bsr
+from workloads import generate, get_config
+from workloads.configs import Workload
+from workloads.gen import random_workload
+
+pytestmark = pytest.mark.gpu
+
+FAIL_NAME = {oracle.FAIL_MISSING: bsr.BSR_FAIL_MISSING, oracle.FAIL_CORRUPT: bsr.BSR_FAIL_CORRUPT,
+             oracle.FAIL_TIMEOUT: bsr.BSR_FAIL_TIMEOUT, oracle.FAIL_TRANSFER: bsr.BSR_FAIL_TRANSFER,
+             oracle.FAIL_ABORT: bsr.BSR_FAIL_ABORT, oracle.FAIL_NONE: bsr.BSR_FAIL_NONE}
+
+
+def _oracle(wi, W, mutate=None, **kw):
+    case = build_case(wi)
+    n, bm, keys = oracle.probe(case.store, wi.tokens, wi.workload.chunk_tokens, wi.salt)
+    if mutate:
+        mutate(case, keys)
+    res = oracle.windowed_restore(case.layout, case.store, keys, n, W, wi.block_tables,
+                                  case.pools, case.valid, **kw)
+    return case, n, bm, keys, res
+
+
+def _compare_success(gc, case, res, out, full_pools=True):
+    G = len(gc.wi.workload.groups)
+    assert out.window_errors == []
+    assert out.exposed_tokens == res.exposed_tokens
+    assert out.fallback == res.fallback == 0
+    st = out.stats
+    assert st["h2d_bytes"] == res.h2d_bytes
+    assert st["installed_bytes"] == res.installed_bytes
+    assert st["peak_live_staging_bytes"] == res.peak_live_staging_bytes
+    assert st["n_windows"] == res.n_windows
+    assert out.status["fail"] == 0 and out.status["phase"] == 2
+    assert out.status["q"][:G] == res.q
+    for g in range(G):
+        np.testing.assert_array_equal(gc.valid_host(g), case.valid[g])
+        if full_pools:
+            np.testing.assert_array_equal(gc.pool_host(g), case.pools[g])
+
+
+def _compare_failure(gc, case, res, out):
+    wi = gc.wi
+    G = len(wi.workload.groups)
+    assert out.exposed_tokens == res.exposed_tokens == 0
+    assert out.fallback == res.fallback == 1
+    assert out.status["fail"] == FAIL_NAME[res.fail_reason]
+    assert out.status["first_failed_chunk"] == res.first_failed_chunk
+    assert out.status["q"][:G] == res.q
+    n_hit = out.stats["n_hit_chunks"]
+    assert out.stats["installed_bytes"] <= n_hit * case.layout.chunk_payload_bytes
+    for g, spec in enumerate(wi.workload.groups):
+        np.testing.assert_array_equal(gc.valid_host(g), case.valid[g])
+        nreq = oracle.request_blocks(n_hit, wi.workload.chunk_tokens, spec.block_tokens)
+        others = np.setdiff1d(np.arange(wi.pool_blocks[g]), wi.block_tables[g][:nreq])
+        np.testing.assert_array_equal(gc.pool_host(g)[:, others], case.pools[g][:, others])
+
+
+def test_keys_and_probe_bit_exact():
+    wi = generate(get_config(1))
+    gc = GpuCase(wi, W=2)
+    try:
+        case = build_case(wi)
+        n, bm, keys = gc.probe(11)
+        on, obm, okeys = oracle.probe(case.store, wi.tokens, 64, wi.salt)
+        assert n == on == 16
+        np.testing.assert_array_equal(bm, obm)
+        assert [int(k) for k in keys] == okeys
+    finally:
+        gc.close()
+
+
+def test_config1_full_parity():
+    say("case: workload 1, W=2, full parity")
+    wi = generate(get_config(1))
+    case, n, _, _, res = _oracle(wi, 2)
+    gc = GpuCase(wi, W=2)
+    try:
+        assert gc.probe(1)[0] == n == 16
+        out = gc.restore(1, n)
+        _compare_success(gc, case, res, out)
+    finally:
+        gc.close()
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_random_layout_parity(seed):
+    w = random_workload(seed)
+    wi = generate(w)
+    for W in w.windows:
+        say(f"case: random layout seed={seed} W={W} groups={[(s.kind, s.block_tokens, s.record_bytes) for s in w.groups]} C={w.chunk_tokens}")
+        case, n, _, _, res = _oracle(wi, W)
+        gc = GpuCase(wi, W=W)
+        try:
+            assert gc.probe(5)[0] == n
+            out = gc.restore(5, n)
+            _compare_success(gc, case, res, out)
+        finally:
+            gc.close()
+
+
+@pytest.mark.parametrize("batch", [1, 3, 16])
+def test_config2_full_parity(batch):
+    say(f"case: workload 2 (32K), W=32, install batch {batch}, full parity")
+    wi = generate(get_config(2))
+    case, n, _, _, res = _oracle(wi, 32)
+    gc = GpuCase(wi, W=32, install_batch=batch)
+    try:
+        assert gc.probe(2)[0] == n == 128
+        out = gc.restore(2, n)
+        _compare_success(gc, case, res, out)
+        assert out.stats["staging_required_bytes"] == 32 * 9_707_520 == 310_640_640
+    finally:
+        gc.close()
+
+
+@pytest.mark.parametrize("mode,k", [("missing", 0), ("missing", 5), ("corrupt", 1), ("corrupt", 15),
+                                    ("timeout", 7), ("transfer", 3), ("abort", 2)])
+def test_config1_failure_parity(mode, k):
+    say(f"case: workload 1 failure {mode} at {k}")
+    wi = generate(get_config(1))
+    kw = {}
+    gkw = {}
+    if mode == "missing":
+        mut = lambda case, keys: case.store.remove(keys[k], 0)  # noqa: E731
+    elif mode == "corrupt":
+        mut = lambda case, keys: case.store.corrupt(keys[k], 0, 777, 0x24)  # noqa: E731
+    else:
+        mut = None
+    if mode == "timeout":
+        kw["faults"] = {k: oracle.FAIL_TIMEOUT}
+    if mode == "transfer":
+        kw["faults"] = {k: oracle.FAIL_TRANSFER}
+    if mode == "abort":
+        kw["abort_after_windows"] = k
+    case, n, _, okeys, res = _oracle(wi, 2, mutate=mut, **kw)
+    gc = GpuCase(wi, W=2, timeout_ms=50 if mode == "timeout" else 0)
+    try:
+        n_g, _, keys = gc.probe(3)
+        if mode == "missing":
+            bsr.bsr_store_remove(gc.ctx, int(keys[k]), 0)
+        elif mode == "corrupt":
+            gc.corrupt(int(keys[k]), 0, 777, 0x24)
+        elif mode == "timeout":
+            bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_DELAY_MS, k, 200)
+        elif mode == "transfer":
+            bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_TRANSFER_ERROR, k, 0)
+        out = gc.restore(3, n_g, abort_after_windows=kw.get("abort_after_windows"))
+        _compare_failure(gc, case, res, out)
+        # force-local: the next admission sees no external tokens until RUNNING/teardown
+        assert gc.probe(3)[0] == 0
+        bsr.bsr_request_running(gc.ctx, 3)
+        assert gc.probe(3)[0] == oracle.probe(case.store, wi.tokens, 64, wi.salt)[0]
+        bsr.bsr_request_end(gc.ctx, 3)
+    finally:
+        gc.close()
+
+
+def test_group_fault_collapses_all_groups_and_mark_invalid():
+    say("case: workload-2 layout, 6 chunks, group B missing at 3; then group marked invalid")
+    w0 = get_config(2)
+    w = Workload(index=2, name="c2-small", n_tokens=6 * 256, chunk_tokens=256,
+                 groups=w0.groups, windows=(2,), base_records=w0.base_records)
+    wi = generate(w)
+    case, n, _, _, res = _oracle(wi, 2, mutate=lambda c, keys: c.store.remove(keys[3], 1))
+    gc = GpuCase(wi, W=2)
+    try:
+        n_g, _, keys = gc.probe(4)
+        bsr.bsr_store_remove(gc.ctx, int(keys[3]), 1)
+        out = gc.restore(4, n_g)
+        _compare_failure(gc, case, res, out)
+        assert out.window_errors == [(2, bsr.BSR_E_MISSING)]
+        bsr.bsr_request_end(gc.ctx, 4)
+    finally:
+        gc.close()
+    # engine-reported invalid group, no window failure (Eq. 6's q_g term)
+    case, n, _, _, res = _oracle(wi, 2, invalid_groups=[1])
+    gc = GpuCase(wi, W=2)
+    try:
+        n_g = gc.probe(6)[0]
+        out = gc.restore(6, n_g, before_commit=lambda: bsr.bsr_mark_group_invalid(gc.ctx, 6, 1))
+        assert res.fail_reason == oracle.FAIL_NONE
+        _compare_failure(gc, case, res, out)
+    finally:
+        gc.close()
+
+
+def test_empty_prefix_and_new_salt():
+    wi = generate(get_config(1))
+    gc = GpuCase(wi, W=2)
+    try:
+        n, bm, _ = gc.probe(8, salt=wi.salt + 2)
+        assert n == 0 and not bm.any()
+        out = gc.restore(8, 0)
+        assert out.exposed_tokens == 0 and out.fallback == 0
+        for g in range(1):
+            np.testing.assert_array_equal(gc.valid_host(g), wi.valid_init[g])
+            np.testing.assert_array_equal(gc.pool_host(g), wi.sentinel_pool(g))
+    finally:
+        gc.close()
