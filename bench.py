@@ -1,0 +1,288 @@
+"""Benchmark of the bounded-window restore path on one MI355X.
+
+One step = one pass of the whole path over one request: probe (chunk keys +
+store lookup), bind (begin kernel), every window's pinned-host -> ring copies
+and install + verify kernels, and the device commit, ending when commit has
+returned to the host.  The external tier is the library's pinned-host store,
+filled before timing; destination pools are resident in HBM.
+
+Prints ONE JSON line.  ``value`` is restored KV bytes per second (1e9 B/s):
+n_hit x (bytes of one chunk's entries) x steps / timed seconds.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=5, choices=[2, 3, 4, 5])
+    ap.add_argument("--window", type=int, default=32)
+    ap.add_argument("--install-batch", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (for counter calibration)")
+    ap.add_argument("--held-chunks", type=int, default=0,
+                    help="profiling passes only: hold just the first N chunks (same launch shape)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (--gpus {args.gpus} "
+              "requested); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_17826_amd import bsr
+    from paper_2608_17826_amd.session import RestoreSession, group_dsts
+    from workloads import generate, get_config
+    from workloads.device import place
+
+    w = get_config(args.workload)
+    W = args.window
+    log(f"[bench] workload {w.index} {w.name}: generating inputs")
+    wi = generate(w)
+    kinds = {"contig": bsr.BSR_KIND_CONTIG, "planar": bsr.BSR_KIND_PLANAR}
+    layout = bsr.make_layout(w.chunk_tokens, [(s.block_tokens, s.n_tensors, s.record_bytes, kinds[s.kind],
+                                               s.split_bytes) for s in w.groups])
+    ctx = bsr.bsr_ctx_create(layout, W, hip_device=0, install_batch=args.install_batch,
+                             flags=bsr.BSR_FLAG_TIME_INSTALL)
+    slot = bsr.bsr_slot_bytes(layout)
+    stride = (slot + 4095) // 4096 * 4096
+    held = w.held_chunks if not args.held_chunks else min(args.held_chunks, w.held_chunks)
+    log(f"[bench] pinned store: {held} chunks x {slot} B")
+    bsr.bsr_store_reserve(ctx, stride * (held + 1))
+    keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
+
+    def put(i):
+        bsr.bsr_store_put_chunk(ctx, int(keys[i]), wi.payloads(i))
+
+    t0 = time.time()
+    with ThreadPoolExecutor(8) as ex:
+        list(ex.map(put, range(held)))
+    log(f"[bench] store filled in {time.time() - t0:.1f}s")
+    dev = place(wi)
+    torch.cuda.synchronize()
+    dsts = group_dsts(dev.block_tables, dev.tensor_bases, dev.valid, wi.pool_blocks)
+
+    sess = RestoreSession(ctx)
+    # the ring alone, allocated the way the session allocates it
+    mem0 = torch.cuda.memory_allocated()
+    probe_ring = torch.empty(bsr.bsr_staging_bytes(layout, W), dtype=torch.uint8, device="cuda")
+    ring_delta = torch.cuda.memory_allocated() - mem0
+    del probe_ring
+    chunk_payload = sum(s.n_tensors * w.chunk_tokens * s.record_bytes for s in w.groups)
+
+    log("[bench] measuring pinned H2D bandwidth (1 GiB, best of 10, 1 and 2 streams)")
+    h2d = max(bsr.bsr_measure_h2d(ctx, 1 << 30, 1, 10), bsr.bsr_measure_h2d(ctx, 1 << 30, 2, 10))
+
+    def step(rid):
+        n, _, _ = bsr.bsr_probe(ctx, rid, wi.salt, wi.tokens)
+        t_r = time.perf_counter()
+        out = sess.restore(rid, n, dsts)
+        t_c = time.perf_counter()
+        bsr.bsr_request_end(ctx, rid)
+        assert out.fallback == 0 and out.exposed_tokens == n * w.chunk_tokens, out
+        return n, out, t_c - t_r
+
+    for i in range(args.warmup):
+        log(f"[bench] warmup step {i}")
+        step(1000 + i)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    outs = []
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        outs.append(step(2000 + i))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    log(f"[bench] timed {args.steps} steps in {elapsed:.3f}s")
+
+    n = outs[0][0]
+    restored = n * chunk_payload
+    value = restored * args.steps / elapsed / 1e9
+    restore_only = restored * args.steps / sum(o[2] for o in outs) / 1e9
+    launches = sum(o[1].stats["n_install_launches"] for o in outs)
+    kern_ms = sum(o[1].stats["install_ms_total"] for o in outs)
+    installed = sum(o[1].stats["installed_bytes"] for o in outs)
+    avg_launch_ms = kern_ms / launches
+    bytes_per_launch = 2 * installed / launches        # read staged + write paged
+    achieved = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
+    st = outs[-1][1].stats
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    traffic, traffic_src = recorded_traffic(w.name, st["install_batch"])
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wi, W, args.cpu_seconds)
+
+    line = {
+        "metric": "restored KV GB/s per GPU (512K tokens, W=32) + peak staging bytes; % H2D/HBM roofline",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: {w.n_tokens} tokens, {n} chunks of {w.chunk_tokens} tokens restored, "
+                        f"{len(w.groups)} groups / {sum(s.n_tensors for s in w.groups)} tensors, W={W}, "
+                        "pinned-host tier -> W-slot HBM ring -> paged pools",
+            "tokens": w.n_tokens, "chunks_restored": n, "window_chunks": W,
+            "chunk_bytes": slot, "restored_bytes_per_step": restored,
+            "install_batch": st["install_batch"],
+            "profiling_subset": bool(args.held_chunks),
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "k_install",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "traffic_source": traffic_src,
+            "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(avg_launch_ms * 1e3, 2),
+            "launches_timed": launches,
+        },
+        "host_link": {
+            "achieved": round(value, 3), "peak_measured": round(h2d, 3), "unit": "GB/s",
+            "frac": round(value / h2d, 4), "restore_only_gbps": round(restore_only, 3),
+            "measured_as": "best of 10 hipMemcpyAsync of 1 GiB from hipHostMalloc memory, 1 and 2 streams",
+        },
+        "staging": {
+            "peak_live_staging_bytes": st["peak_live_staging_bytes"],
+            "ring_bytes_allocated": int(ring_delta),
+            "law_W_times_chunk_bytes": W * slot,
+            "aux_device_bytes": st["aux_device_bytes"],
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    bsr.bsr_ctx_destroy(ctx)
+
+
+def kernel_sources_sha256():
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload_name, install_batch):
+    """HBM bytes per k_install launch from the committed rocprofv3 counter
+    summary, only if it was taken on the kernel sources built here."""
+    import glob
+    import re
+
+    sha = kernel_sources_sha256()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+        for m in re.finditer(r"<!-- traffic-record ([^>]*) -->", open(path).read()):
+            kv = dict(x.split("=", 1) for x in m.group(1).split())
+            if (kv.get("kernel") == "k_install" and kv.get("workload") == workload_name
+                    and int(kv.get("install_batch", -1)) == install_batch
+                    and kv.get("kernel_sources_sha256") == sha):
+                return int(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+    return None, None
+
+
+def cpu_baseline(wi, W, target_s):
+    """The oracle, single-threaded, on the first windows of the same workload.
+
+    The sample restores whole windows (W chunks each) until about target_s
+    seconds of oracle work; destination pools are compacted to the blocks
+    the sample touches (block ids renumbered), which changes no arithmetic.
+    """
+    import numpy as np
+
+    import oracle
+
+    w = wi.workload
+    layout = oracle.OracleLayout.from_specs(w.chunk_tokens, w.groups)
+    t0 = time.perf_counter()
+    keys = oracle.chain_keys(wi.tokens, w.chunk_tokens, wi.salt)
+    t_keys = time.perf_counter() - t0
+    done, t_restore, windows = 0, 0.0, 0
+    while t_restore < target_s and done < w.held_chunks:
+        k = min(W, w.held_chunks - done)
+        # a store holding this window's chunks, and compact pools
+        store = oracle.OracleStore(layout.n_groups)
+        for i in range(done, done + k):
+            store.put_chunk(keys[i], wi.payloads(i))
+        bts, pools, valid = [], [], []
+        for g, spec in enumerate(w.groups):
+            lo = done * w.chunk_tokens // spec.block_tokens
+            hi = -(-((done + k) * w.chunk_tokens) // spec.block_tokens)
+            bt = np.full(hi, -1, dtype=np.int64)
+            bt[lo:hi] = np.arange(hi - lo)
+            bts.append(bt)
+            pools.append(np.zeros((spec.n_tensors, hi - lo, layout.block_bytes(g)), np.uint8))
+            valid.append(np.zeros(hi - lo, np.uint8))
+        sub_keys = [None] * done + keys[done:done + k]
+        t1 = time.perf_counter()
+        res = _restore_range(layout, store, sub_keys, done, k, W, bts, pools, valid)
+        t_restore += time.perf_counter() - t1
+        assert res.fail_reason == 0
+        done += k
+        windows += 1
+    restored = done * layout.chunk_payload_bytes
+    probe_share = t_keys * done / max(1, len(keys))
+    return {"value": round(restored / (t_restore + probe_share) / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"first {done} of {w.held_chunks} chunks ({windows} windows of W={W}); "
+                      f"{restored} bytes in {t_restore:.1f}s + pro-rated probe {probe_share:.2f}s"}
+
+
+def _restore_range(layout, store, keys, first, k, W, bts, pools, valid):
+    """Oracle windowed restore of chunks [first, first + k) (one window)."""
+    import oracle
+
+    # the oracle restores a prefix from chunk 0; shift the plan so the sample
+    # window is its only window
+    shifted_keys = keys[first:first + k]
+    shifted_bts = []
+    C = layout.chunk_tokens
+    for g, gr in enumerate(layout.groups):
+        lo_tok = first * C
+        if lo_tok % gr.block_tokens == 0:
+            shifted_bts.append(bts[g][lo_tok // gr.block_tokens:])
+        else:
+            raise ValueError("sample windows must start on a block boundary")
+    return oracle.windowed_restore(layout, store, shifted_keys, k, W, shifted_bts, pools, valid)
+
+
+if __name__ == "__main__":
+    main()

@@ -11,9 +11,25 @@
 
 namespace bsr {
 
-constexpr int kInstallThreads = 256;     // 4 wave64 per workgroup
-constexpr uint32_t kPieceBytes = 16384;  // contiguous-group bytes per workgroup
-constexpr uint32_t kLdsCapBytes = 32768; // planar pieces staged through LDS up to this size
+#ifndef BSR_MAX_PIECE_BYTES
+#define BSR_MAX_PIECE_BYTES 8192
+#endif
+#ifndef BSR_PLANAR_PIECE_BYTES
+#define BSR_PLANAR_PIECE_BYTES 20480
+#endif
+
+#ifndef BSR_INSTALL_THREADS
+#define BSR_INSTALL_THREADS 256
+#endif
+
+constexpr int kInstallThreads = BSR_INSTALL_THREADS;  // wave64 multiples
+constexpr int kInstallWaves = kInstallThreads / 64;
+// contiguous segments are cut into equal pieces of at most this many bytes,
+// each a multiple of 4 KiB (one 16-byte vector per thread per 4 KiB)
+constexpr uint32_t kMaxPieceBytes = BSR_MAX_PIECE_BYTES;
+constexpr uint32_t kPieceAlign = 16 * kInstallThreads;
+// planar pieces (whole tokens) are staged through LDS up to this size
+constexpr uint32_t kLdsCapBytes = BSR_PLANAR_PIECE_BYTES;
 
 // Tag partial of one install workgroup: sum and XOR of the little-endian u32
 // words it read from the staged chunk.
@@ -21,6 +37,27 @@ struct TagPair {
   uint32_t sum;
   uint32_t x;
 };
+
+// Division of a 32-bit n by an invariant d as a multiply-high and two
+// shifts (Granlund & Montgomery, "Division by invariant integers using
+// multiplication", 1994, round-up multiplier): t = mulhi(m, n),
+// n / d = (t + ((n - t) >> s1)) >> s2.  Built on the host (make_fastdiv).
+struct FastDiv {
+  uint32_t d, m, s1, s2;
+#if defined(__HIP__)
+  __host__ __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    const uint32_t t = static_cast<uint32_t>((static_cast<uint64_t>(m) * n) >> 32);
+    return (t + ((n - t) >> s1)) >> s2;
+  }
+#endif
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;  // l = ceil(log2 d)
+  const uint64_t m = ((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d) + 1;
+  return FastDiv{d, static_cast<uint32_t>(m), l < 1 ? l : 1u, l > 1 ? l - 1 : 0u};
+}
 
 // Per-group geometry of one install launch.
 struct GroupGeom {
@@ -38,12 +75,17 @@ struct GroupGeom {
   uint32_t n_blocks;
   const int32_t* block_table;
   uint8_t* const* tensor_bases;
+  FastDiv div_pieces;       // by pieces_per_seg
+  FastDiv div_segs;         // by segs_per_chunk
+  FastDiv div_per_chunk;    // by the group's workgroups per chunk
+  FastDiv div_block;        // by block_tokens
 };
 
 struct InstallParams {
   const uint8_t* ring;
   uint64_t slot_bytes;
   uint32_t window;          // W (slots in the ring)
+  FastDiv div_window;       // by W
   uint32_t chunk_tokens;
   uint32_t n_groups;
   uint32_t n_chunks;        // chunks in this launch (<= BSR_MAX_INSTALL_BATCH)
@@ -51,14 +93,27 @@ struct InstallParams {
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
   uint32_t wg_start[BSR_MAX_GROUPS + 1];  // prefix of workgroups per group within a chunk
   uint32_t lds_bytes;       // dynamic LDS of this launch
+  // Dispatch order: workgroups are issued group by group (slowest pieces
+  // first, so the launch's tail is made of the shortest pieces); within a
+  // group, chunk by chunk.  Tag partials keep their chunk-major slot.
+  uint32_t order[BSR_MAX_GROUPS];
   GroupGeom g[BSR_MAX_GROUPS];
-  TagPair* partials;        // [n_chunks * wg_per_chunk], one per workgroup
+  TagPair* partials;        // [n_chunks * wg_per_chunk * kInstallWaves], one per wave
   const bsr_dev_status* status;
+};
+
+// Device words the verify kernel uses across workgroups (library-owned,
+// zeroed by the begin kernel and left zeroed by every verify launch).
+struct VerifyAux {
+  uint32_t bad[BSR_MAX_INSTALL_BATCH];  // per chunk of the launch: mask of mismatching groups
+  uint32_t arrivals;                    // workgroups finished in the current launch
+  uint32_t pad[15];
 };
 
 struct VerifyParams {
   const TagPair* partials;
   bsr_dev_status* status;
+  VerifyAux* aux;
   uint32_t n_chunks;
   uint32_t first_chunk;
   uint32_t n_groups;
@@ -84,6 +139,7 @@ enum FinishMode : uint32_t {
 
 struct FinishParams {
   bsr_dev_status* status;
+  VerifyAux* verify_aux;    // begin: zeroed
   uint32_t mode;
   uint32_t n_groups;
   uint32_t reason;          // invalidate: BSR_FAIL_*
@@ -94,7 +150,8 @@ struct FinishParams {
   GroupValid g[BSR_MAX_GROUPS];
 };
 
-hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s);
+hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s,
+                          hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_verify(const VerifyParams& p, hipStream_t s);
 hipError_t launch_finish(const FinishParams& p, hipStream_t s);
 

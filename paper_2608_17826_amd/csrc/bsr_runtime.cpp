@@ -146,6 +146,7 @@ struct Geometry {
   uint32_t wg_start[BSR_MAX_GROUPS + 1]{};
   uint32_t wg_per_chunk = 0;
   uint32_t lds_bytes = 0;
+  uint32_t order[BSR_MAX_GROUPS]{};  // install dispatch order of the groups
 };
 
 int check_layout(const bsr_layout* L) {
@@ -198,8 +199,10 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
       q.segs_per_chunk = (C + B - 1) / B + 1;
     const uint32_t seg_tokens = std::min(B, C);
     if (d.kind == BSR_KIND_CONTIG) {
+      // equal pieces of at most kMaxPieceBytes, each a multiple of 4 KiB
       const uint64_t seg = static_cast<uint64_t>(seg_tokens) * d.record_bytes;
-      q.piece_bytes = bsr::kPieceBytes;
+      const uint64_t n = (seg + bsr::kMaxPieceBytes - 1) / bsr::kMaxPieceBytes;
+      q.piece_bytes = static_cast<uint32_t>(align_up((seg + n - 1) / n, bsr::kPieceAlign));
       q.pieces_per_seg = static_cast<uint32_t>((seg + q.piece_bytes - 1) / q.piece_bytes);
       q.piece_tokens = 0;
     } else {
@@ -212,14 +215,26 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
       q.pieces_per_seg = (seg_tokens + pt - 1) / pt;
       q.piece_bytes = 0;
       const uint32_t need = static_cast<uint32_t>(align_up(static_cast<uint64_t>(pt) * d.record_bytes, 16));
-      if (need <= bsr::kLdsCapBytes) G->lds_bytes = std::max(G->lds_bytes, need);
+      if (need <= bsr::kLdsCapBytes) G->lds_bytes = std::max(G->lds_bytes, need);  // else: 4-byte word path
     }
     G->wg_start[g] = wg;
     wg += d.n_tensors * q.segs_per_chunk * q.pieces_per_seg;
+    q.div_pieces = bsr::make_fastdiv(q.pieces_per_seg);
+    q.div_segs = bsr::make_fastdiv(q.segs_per_chunk);
+    q.div_per_chunk = bsr::make_fastdiv(d.n_tensors * q.segs_per_chunk * q.pieces_per_seg);
+    q.div_block = bsr::make_fastdiv(B);
   }
   G->wg_start[L->n_groups] = wg;
   for (uint32_t g = L->n_groups + 1; g <= BSR_MAX_GROUPS; ++g) G->wg_start[g] = wg;
   G->wg_per_chunk = wg;
+  // dispatch planar groups first (LDS-staged, slowest per byte), then
+  // contiguous groups by descending piece size
+  for (uint32_t g = 0; g < L->n_groups; ++g) G->order[g] = g;
+  auto cost = [&](uint32_t g) -> uint64_t {
+    const GroupGeom& q = G->gg[g];
+    return q.kind == BSR_KIND_PLANAR ? (1ull << 40) : q.piece_bytes;
+  };
+  std::stable_sort(G->order, G->order + L->n_groups, [&](uint32_t a, uint32_t b) { return cost(a) > cost(b); });
   G->slot_bytes = off;
   G->chunk_payload = 0;
   for (uint32_t g = 0; g < L->n_groups; ++g) G->chunk_payload += G->payload[g];
@@ -327,8 +342,9 @@ struct bsr_ctx {
   bsr_stats stats{};
   Inject inject;
   // device resources
-  TagPair* partials = nullptr;
+  TagPair* partials = nullptr;      // per-wave tag partials of one install launch
   uint64_t partials_bytes = 0;
+  bsr::VerifyAux* verify_aux = nullptr;
   bsr_dev_status* host_status = nullptr;  // pinned mirror
   std::vector<hipEvent_t> full_ev, free_ev, start_ev;
   std::vector<hipEvent_t> timing_pool;
@@ -384,17 +400,15 @@ int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::arra
   if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
     t1 = take_timing_event(c);
-    if (t0 && t1) (void)hipEventRecord(t0, s.compute);
+    if (!t0 || !t1) t0 = t1 = nullptr;
   }
-  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute), "install launch")))
+  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute, t0, t1), "install launch")))
     return rc;
-  if (t0 && t1) {
-    (void)hipEventRecord(t1, s.compute);
-    s.timing.emplace_back(t0, t1);
-  }
+  if (t0 && t1) s.timing.emplace_back(t0, t1);
   VerifyParams vp{};
   vp.partials = c->partials;
   vp.status = s.status;
+  vp.aux = c->verify_aux;
   vp.n_chunks = ip.n_chunks;
   vp.first_chunk = ip.first_chunk;
   vp.n_groups = c->geo.L.n_groups;
@@ -519,11 +533,12 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
       delete c;
       return rc;
     }
-    c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * sizeof(TagPair);
+    c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
     const uint32_t E = W + 2;
     c->full_ev.assign(E, nullptr);
     c->free_ev.assign(E, nullptr);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->partials), c->partials_bytes) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->verify_aux), sizeof(bsr::VerifyAux)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
     for (uint32_t i = 0; ok && i < E; ++i)
       ok = hipEventCreateWithFlags(&c->full_ev[i], hipEventDisableTiming) == hipSuccess &&
@@ -532,7 +547,7 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
       bsr_ctx_destroy(c);
       return fail_with(BSR_E_NOMEM, "device resources for W=%u could not be allocated", W);
     }
-    c->stats.aux_device_bytes = c->partials_bytes;
+    c->stats.aux_device_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
   }
   *out = c;
   return BSR_OK;
@@ -557,6 +572,7 @@ int bsr_ctx_destroy(bsr_ctx* c) {
     }
     for (auto e : c->timing_pool) (void)hipEventDestroy(e);
     if (c->partials) (void)hipFree(c->partials);
+    if (c->verify_aux) (void)hipFree(c->verify_aux);
     if (c->host_status) (void)hipHostFree(c->host_status);
     if (c->store.owned && c->store.arena) (void)hipHostFree(c->store.arena);
   }
@@ -732,6 +748,8 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   Request& rq = it->second;
   if (rq.phase != Phase::Probed) return fail_with(BSR_E_STATE, "request %llu already bound once; probe again", (unsigned long long)request_id);
   if (n_hit > rq.n_probe) return fail_with(BSR_E_ARG, "n_hit_chunks %u exceeds the probed prefix %u", n_hit, rq.n_probe);
+  if (static_cast<uint64_t>(n_hit) * c->geo.L.chunk_tokens >= (1ull << 32))
+    return fail_with(BSR_E_ARG, "a restored prefix must be shorter than 2^32 tokens");
   if (!dst || !staging || !status) return fail_with(BSR_E_ARG, "dst, staging or status is NULL");
   if (!copy_stream || !compute_stream || copy_stream == compute_stream)
     return fail_with(BSR_E_ARG, "copy and compute streams must be distinct non-null streams");
@@ -744,16 +762,19 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   hipStream_t compute = static_cast<hipStream_t>(compute_stream);
   FinishParams fp{};
   fp.status = status;
+  fp.verify_aux = c->verify_aux;
   fp.n_groups = G;
   fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
   InstallParams ip{};
   ip.ring = static_cast<const uint8_t*>(staging);
   ip.slot_bytes = c->geo.slot_bytes;
   ip.window = c->W;
+  ip.div_window = bsr::make_fastdiv(c->W);
   ip.chunk_tokens = C;
   ip.n_groups = G;
   ip.wg_per_chunk = c->geo.wg_per_chunk;
   std::memcpy(ip.wg_start, c->geo.wg_start, sizeof ip.wg_start);
+  std::memcpy(ip.order, c->geo.order, sizeof ip.order);
   ip.lds_bytes = c->geo.lds_bytes;
   ip.partials = c->partials;
   ip.status = status;
