@@ -172,7 +172,11 @@ class RestoreResult:
     trace: List[int] = field(default_factory=list)
 
 
-def _set_request_valid(layout, n_hit, block_tables, valid, value) -> None:
+def set_request_valid(layout: OracleLayout, n_hit: int, block_tables: Sequence[np.ndarray],
+                      valid: Sequence[np.ndarray], value: int) -> None:
+    """Set the validity byte of every block the advertised prefix touches, in
+    every group (bind clears them; commit sets them to Q, §3 Eq. 6 and §4
+    failed-block / HMA-aware invalidation)."""
     for g, gr in enumerate(layout.groups):
         for k in range(request_blocks(n_hit, layout.chunk_tokens, gr.block_tokens)):
             valid[g][int(block_tables[g][k])] = value
@@ -204,7 +208,7 @@ def windowed_restore(layout: OracleLayout, store: OracleStore, keys: Sequence[in
     staging = np.zeros((n_slots, slot_bytes), dtype=np.uint8)   # the local restore pool
 
     # bind: the advertised blocks hold no valid state until commit
-    _set_request_valid(layout, n_hit, block_tables, valid, 0)
+    set_request_valid(layout, n_hit, block_tables, valid, 0)
 
     fail, first_failed, q = FAIL_NONE, NO_CHUNK, [1] * G
     for g in invalid_groups:
@@ -256,10 +260,10 @@ def windowed_restore(layout: OracleLayout, store: OracleStore, keys: Sequence[in
     # commit (Eq. 6, one rank): all groups valid and no window failed
     Q = fail == FAIL_NONE and all(q)
     if Q:
-        _set_request_valid(layout, n_hit, block_tables, valid, 1)
+        set_request_valid(layout, n_hit, block_tables, valid, 1)
         exposed, fallback = n_hit * C, 0
     else:
-        _set_request_valid(layout, n_hit, block_tables, valid, 0)
+        set_request_valid(layout, n_hit, block_tables, valid, 0)
         exposed, fallback = 0, 1
     return RestoreResult(exposed, fallback, fail, first_failed, q, n_windows, peak, h2d,
                          installed, trace)

@@ -75,3 +75,20 @@ class GeneratorStore:
     def remove(self, key: int, g: int = -1) -> None:
         for gg in (range(self.n_groups) if g < 0 else [g]):
             self.removed.add((int(key), gg))
+
+
+class _SinkTensor:
+    def __init__(self, block_bytes: int):
+        self.scratch = np.zeros(block_bytes, np.uint8)
+
+    def __getitem__(self, idx):
+        return self.scratch
+
+
+class SinkPools(list):
+    """Destination pools that accept every block write into one scratch block
+    per group: lets the oracle walk a full-size failing restore (whose pool
+    contents are unspecified) for its metadata without a 40-70 GB image."""
+
+    def __init__(self, wi: WorkloadInputs):
+        super().__init__(_SinkTensor(wi.block_bytes(g)) for g in range(len(wi.workload.groups)))
