@@ -196,7 +196,8 @@ def kernel_sources_sha256():
     import hashlib
 
     h = hashlib.sha256()
-    for f in ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h"):
+    for f in ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h",
+              "include/bsr.h"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()

@@ -59,7 +59,7 @@ extern "C" {
 
 #define BSR_ABI_VERSION 1
 #define BSR_MAX_GROUPS 8
-#define BSR_MAX_INSTALL_BATCH 16
+#define BSR_MAX_INSTALL_BATCH 32
 #define BSR_NO_CHUNK 0xFFFFFFFFu
 
 /* status codes */
@@ -119,7 +119,9 @@ typedef struct bsr_layout {
 
 typedef struct bsr_config {
   uint32_t window_chunks;     /* W >= 1: staging slots, the restore-window size */
-  uint32_t install_batch;     /* chunks per install launch, 0 = automatic; <= min(W, BSR_MAX_INSTALL_BATCH) */
+  uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W - W/8, at least 1, at most
+                                 BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
+                                 windows; a batch smaller than W keeps the copy engine busy across windows */
   int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
   uint32_t flags;             /* BSR_FLAG_* */
   uint32_t window_timeout_ms; /* per-window fetch deadline, 0 = none */
@@ -287,8 +289,11 @@ int bsr_request_bind(bsr_ctx* ctx, uint64_t request_id, uint32_t n_hit_chunks,
  * (a missing entry, an injected delay beyond the window deadline, or a
  * failed copy submission fails the window), waits for the chunk's slot to be
  * released, and enqueues the pinned-host -> slot copy on copy_stream; per
- * install batch it enqueues the install and verify kernels on
- * compute_stream and releases the batch's slots behind them.  On a
+ * install batch (which may span windows: chunks left over at the end of a
+ * call join the next call's batch, and every later call of the request --
+ * commit, invalidate, mark, end -- installs them first) it enqueues the
+ * install and verify kernels on compute_stream and releases the batch's
+ * slots behind them.  On a
  * host-detected failure it enqueues the chunks before the failing one, then
  * an invalidate, and returns BSR_E_MISSING / BSR_E_TIMEOUT /
  * BSR_E_TRANSFER; later windows return BSR_E_STATE.  Device-detected

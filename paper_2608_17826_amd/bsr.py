@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbsr.so")
 
 BSR_MAX_GROUPS = 8
-BSR_MAX_INSTALL_BATCH = 16
+BSR_MAX_INSTALL_BATCH = 32
 BSR_NO_CHUNK = 0xFFFFFFFF
 
 BSR_OK = 0

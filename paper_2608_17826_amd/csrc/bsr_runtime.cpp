@@ -318,6 +318,9 @@ struct Session {  // the bound request
   uint32_t slots_touched = 0;
   std::vector<uint8_t> slot_used;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> timing;
+  // chunks copied but not yet installed (the current install batch)
+  std::vector<uint32_t> pend;
+  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>> pend_tags;
 };
 
 struct Inject {
@@ -427,6 +430,8 @@ int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::arra
 }
 
 int enqueue_finish(bsr_ctx* c, uint32_t mode, uint32_t reason, uint32_t chunk, uint32_t mask) {
+  // chunks still waiting for their install go first (stream order)
+  if (int rc = flush_batch(c, c->s.pend, c->s.pend_tags)) return rc;
   FinishParams fp = c->s.fp;
   fp.mode = mode;
   fp.reason = reason;
@@ -506,7 +511,9 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
     return fail_with(BSR_E_ARG, "config.reserved must be 0");
   const uint32_t W = config->window_chunks;
   uint32_t b = config->install_batch;
-  if (b == 0) b = std::max(1u, std::min(W / 2, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
+  // automatic: W - W/8 chunks per launch (at least 1): large launches, and
+  // W/8 chunk-copies of slack before a slot's next copy needs its install
+  if (b == 0) b = std::max(1u, std::min(W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
   if (b > W || b > BSR_MAX_INSTALL_BATCH)
     return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
 
@@ -869,10 +876,12 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   const uint32_t G = c->geo.L.n_groups;
   const uint32_t all_mask = (G >= 32) ? 0xFFFFFFFFu : ((1u << G) - 1);
   const uint32_t E = static_cast<uint32_t>(c->free_ev.size());
-  std::vector<uint32_t> batch;
-  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>> tags;
-  batch.reserve(c->batch);
-  tags.reserve(c->batch);
+  // The install batch may span windows.  A copy into slot i mod W needs the
+  // install of chunk i - W, which is never in the pending batch (it holds at
+  // most install_batch - 1 <= W - 1 earlier chunks), so its release event has
+  // been recorded already.
+  std::vector<uint32_t>& batch = s.pend;
+  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags = s.pend_tags;
   const uint64_t t_window = now_ns();
   int rc = BSR_OK;
 
@@ -950,7 +959,8 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     if (batch.size() == c->batch)
       if ((rc = flush_batch(c, batch, tags))) return rc;
   }
-  if ((rc = flush_batch(c, batch, tags))) return rc;
+  if (first_chunk + n_chunks == s.n_hit)
+    if ((rc = flush_batch(c, batch, tags))) return rc;  // the prefix is complete
   s.next_chunk = first_chunk + n_chunks;
   ++c->stats.n_windows;
   c->stats.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
@@ -991,6 +1001,7 @@ static int complete_session(bsr_ctx* c, bool run_commit, uint64_t* exposed, int3
     }
     if (!rc) rc = enqueue_finish(c, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
   }
+  if (!rc) rc = flush_batch(c, s.pend, s.pend_tags);
   const uint64_t t0 = now_ns();
   if (!rc) rc = hip_check(hipMemcpyAsync(c->host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
   int rc2 = hip_check(hipStreamSynchronize(s.compute), "hipStreamSynchronize(compute)");
