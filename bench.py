@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=5, choices=[2, 3, 4, 5])
-    ap.add_argument("--window", type=int, default=32)
+    ap.add_argument("--window", type=int, default=32, help="W in chunks; 0 = legacy whole-plan mode")
     ap.add_argument("--install-batch", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
@@ -91,7 +91,7 @@ def main():
     sess = RestoreSession(ctx)
     # the ring alone, allocated the way the session allocates it
     mem0 = torch.cuda.memory_allocated()
-    probe_ring = torch.empty(bsr.bsr_staging_bytes(layout, W), dtype=torch.uint8, device="cuda")
+    probe_ring = torch.empty(bsr.bsr_plan_staging_bytes(ctx, held), dtype=torch.uint8, device="cuda")
     ring_delta = torch.cuda.memory_allocated() - mem0
     del probe_ring
     chunk_payload = sum(s.n_tensors * w.chunk_tokens * s.record_bytes for s in w.groups)
@@ -143,7 +143,7 @@ def main():
     traffic, traffic_src = recorded_traffic(w.name, st["install_batch"])
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and W > 0:
         cpu = cpu_baseline(wi, W, args.cpu_seconds)
 
     line = {
@@ -183,7 +183,8 @@ def main():
         "staging": {
             "peak_live_staging_bytes": st["peak_live_staging_bytes"],
             "ring_bytes_allocated": int(ring_delta),
-            "law_W_times_chunk_bytes": W * slot,
+            "law_W_times_chunk_bytes": (W or n) * slot,
+            "mode": "bounded window" if W else "legacy whole-plan (W=0)",
             "aux_device_bytes": st["aux_device_bytes"],
         },
         "cpu_baseline": cpu,

@@ -118,7 +118,9 @@ typedef struct bsr_layout {
 } bsr_layout;
 
 typedef struct bsr_config {
-  uint32_t window_chunks;     /* W >= 1: staging slots, the restore-window size */
+  uint32_t window_chunks;     /* W: staging slots, the restore-window size; 0 = legacy whole-plan mode
+                                 (§4 "Restore-window configuration": each request's ring holds its whole
+                                 plan, n_hit slots, none reused; peak staging n_hit * slot bytes, Eq. 2) */
   uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W - W/8, at least 1, at most
                                  BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
                                  windows; a batch smaller than W keeps the copy engine busy across windows */
@@ -180,6 +182,7 @@ typedef struct bsr_stats {
 
 typedef struct bsr_ctx bsr_ctx;
 
+
 /* ---- library / layout ---------------------------------------------------- */
 
 /* BSR_ABI_VERSION of the loaded library. */
@@ -200,6 +203,10 @@ uint64_t bsr_slot_bytes(const bsr_layout* layout);
 /* Eq. 5 analogue M(W) = W * c: the staging ring size the caller must
  * provide.  0 if the layout is invalid or W == 0. */
 uint64_t bsr_staging_bytes(const bsr_layout* layout, uint32_t window_chunks);
+
+/* Ring bytes a request of n_hit_chunks needs on this context: W * c, or
+ * n_hit_chunks * c in whole-plan mode (W = 0).  0 on a NULL context. */
+uint64_t bsr_plan_staging_bytes(bsr_ctx* ctx, uint32_t n_hit_chunks);
 
 /* Chunk keys of a token sequence (§2 restore plan; the key function is this
  * library's reading, the paper fixes none):
@@ -273,8 +280,8 @@ int bsr_probe(bsr_ctx* ctx, uint64_t request_id, uint64_t salt, const int32_t* t
  * (BSR_E_BUSY if another request holds it).  n_hit_chunks <= the probed n.
  * dst: n_groups destinations (block tables are copied to the host once and
  * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG).
- * staging: device ring of staging_bytes >= W * slot bytes (else
- * BSR_E_STAGING); the library uses exactly W * slot bytes of it.
+ * staging: device ring of staging_bytes >= bsr_plan_staging_bytes(ctx,
+ * n_hit_chunks) (else BSR_E_STAGING); the library uses exactly that many.
  * status: device bsr_dev_status.  Enqueues, on compute_stream, the begin
  * kernel: status reset (fail = 0, q = 1, exposed = 0) and the valid bytes of
  * every advertised block cleared, so no block of the prefix reads valid
@@ -284,7 +291,8 @@ int bsr_request_bind(bsr_ctx* ctx, uint64_t request_id, uint32_t n_hit_chunks,
                      bsr_dev_status* status, void* copy_stream, void* compute_stream);
 
 /* Restore window [first_chunk, first_chunk + n_chunks) of the bound request
- * (§4 windowed retrieve; 1 <= n_chunks <= W, first_chunk = the next chunk not
+ * (§4 windowed retrieve; 1 <= n_chunks <= W (<= n_hit in whole-plan mode),
+ * first_chunk = the next chunk not
  * yet requested).  Asynchronous: for each chunk it looks the entries up
  * (a missing entry, an injected delay beyond the window deadline, or a
  * failed copy submission fails the window), waits for the chunk's slot to be

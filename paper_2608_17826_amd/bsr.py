@@ -94,6 +94,7 @@ def _load() -> ct.CDLL:
         "bsr_last_error": (ct.c_char_p, []),
         "bsr_slot_bytes": (U64, [P(bsr_layout)]),
         "bsr_staging_bytes": (U64, [P(bsr_layout), U32]),
+        "bsr_plan_staging_bytes": (U64, [VP, U32]),
         "bsr_chunk_keys": (ct.c_int, [U64, VP, U64, U32, VP]),
         "bsr_ctx_create": (ct.c_int, [P(bsr_layout), P(bsr_config), P(VP)]),
         "bsr_ctx_destroy": (ct.c_int, [VP]),
@@ -167,6 +168,13 @@ def bsr_slot_bytes(layout: bsr_layout) -> int:
 
 def bsr_staging_bytes(layout: bsr_layout, window_chunks: int) -> int:
     n = _lib.bsr_staging_bytes(ct.byref(layout), window_chunks)
+    if n == 0:
+        raise BsrError(BSR_E_ARG, bsr_last_error())
+    return n
+
+
+def bsr_plan_staging_bytes(ctx: "Ctx", n_hit_chunks: int) -> int:
+    n = _lib.bsr_plan_staging_bytes(ctx, n_hit_chunks)
     if n == 0:
         raise BsrError(BSR_E_ARG, bsr_last_error())
     return n

@@ -303,6 +303,7 @@ struct Session {  // the bound request
   uint64_t id = 0;
   bool active = false;
   uint32_t n_hit = 0;
+  uint32_t window = 0;  // slots of this request's ring: W, or n_hit in whole-plan mode
   uint32_t next_chunk = 0;
   bool failed = false;
   int host_fail = BSR_FAIL_NONE;
@@ -421,7 +422,7 @@ int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::arra
     for (uint32_t g = 0; g < BSR_MAX_GROUPS; ++g) vp.expected[i][g] = tags[i][g];
   if ((rc = hip_check(bsr::launch_verify(vp, s.compute), "verify launch"))) return rc;
   if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
-  for (uint32_t ch : chunks) s.slot_free_seq[ch % c->W] = seq;
+  for (uint32_t ch : chunks) s.slot_free_seq[ch % s.window] = seq;
   c->stats.n_install_launches++;
   c->stats.installed_bytes += static_cast<uint64_t>(chunks.size()) * c->geo.chunk_payload;
   chunks.clear();
@@ -490,6 +491,15 @@ uint64_t bsr_staging_bytes(const bsr_layout* layout, uint32_t window_chunks) {
   return bsr_slot_bytes(layout) * window_chunks;
 }
 
+uint64_t bsr_plan_staging_bytes(bsr_ctx* c, uint32_t n_hit_chunks) {
+  if (!c) {
+    fail_with(BSR_E_ARG, "ctx is NULL");
+    return 0;
+  }
+  const uint64_t slots = c->W ? c->W : std::max(1u, n_hit_chunks);
+  return slots * c->geo.slot_bytes;
+}
+
 int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens, uint32_t chunk_tokens,
                    uint64_t* keys_out) {
   if (!host_is_little_endian()) return fail_with(BSR_E_ARG, "big-endian host unsupported");
@@ -506,15 +516,18 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
-  if (config->window_chunks == 0) return fail_with(BSR_E_ARG, "W (window_chunks) must be >= 1");
   if (config->reserved[0] || config->reserved[1] || config->reserved[2])
     return fail_with(BSR_E_ARG, "config.reserved must be 0");
+  // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
+  // each request's ring holds its whole plan and no slot is reused.
   const uint32_t W = config->window_chunks;
   uint32_t b = config->install_batch;
   // automatic: W - W/8 chunks per launch (at least 1): large launches, and
   // W/8 chunk-copies of slack before a slot's next copy needs its install
-  if (b == 0) b = std::max(1u, std::min(W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
-  if (b > W || b > BSR_MAX_INSTALL_BATCH)
+  if (b == 0)
+    b = W == 0 ? static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)
+               : std::max(1u, std::min(W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
+  if ((W && b > W) || b > BSR_MAX_INSTALL_BATCH)
     return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
 
   auto* c = new (std::nothrow) bsr_ctx();
@@ -541,7 +554,10 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
       return rc;
     }
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
-    const uint32_t E = W + 2;
+    // event ring: the copy of chunk i waits for the release of chunk i - W,
+    // recorded at most W batches earlier (W + 2 leaves a margin); whole-plan
+    // contexts size it per request at bind
+    const uint32_t E = W ? W + 2 : 2;
     c->full_ev.assign(E, nullptr);
     c->free_ev.assign(E, nullptr);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->partials), c->partials_bytes) == hipSuccess &&
@@ -760,7 +776,8 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   if (!dst || !staging || !status) return fail_with(BSR_E_ARG, "dst, staging or status is NULL");
   if (!copy_stream || !compute_stream || copy_stream == compute_stream)
     return fail_with(BSR_E_ARG, "copy and compute streams must be distinct non-null streams");
-  const uint64_t need = c->geo.slot_bytes * c->W;
+  const uint32_t window = c->W ? c->W : std::max(1u, n_hit);
+  const uint64_t need = c->geo.slot_bytes * window;
   if (staging_bytes < need)
     return fail_with(BSR_E_STAGING, "staging %llu B < W x slot = %llu B", (unsigned long long)staging_bytes, (unsigned long long)need);
   if (reinterpret_cast<uintptr_t>(staging) % 256) return fail_with(BSR_E_ARG, "staging must be 256-byte aligned");
@@ -775,8 +792,8 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   InstallParams ip{};
   ip.ring = static_cast<const uint8_t*>(staging);
   ip.slot_bytes = c->geo.slot_bytes;
-  ip.window = c->W;
-  ip.div_window = bsr::make_fastdiv(c->W);
+  ip.window = window;
+  ip.div_window = bsr::make_fastdiv(window);
   ip.chunk_tokens = C;
   ip.n_groups = G;
   ip.wg_per_chunk = c->geo.wg_per_chunk;
@@ -829,9 +846,22 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   s.compute = compute;
   s.ip = ip;
   s.fp = fp;
-  s.slot_free_seq.assign(c->W, -1);
-  s.slot_used.assign(c->W, 0);
+  s.window = window;
+  s.slot_free_seq.assign(window, -1);
+  s.slot_used.assign(window, 0);
 
+  if (c->W == 0) {
+    // whole-plan mode: one event pair per install batch of the plan
+    const uint32_t E = (n_hit + c->batch - 1) / c->batch + 2;
+    while (c->full_ev.size() < E) {
+      hipEvent_t a = nullptr, b2 = nullptr;
+      if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&b2, hipEventDisableTiming) != hipSuccess)
+        return fail_with(BSR_E_NOMEM, "event creation failed");
+      c->full_ev.push_back(a);
+      c->free_ev.push_back(b2);
+    }
+  }
   // begin: reset the status words and clear the advertised valid bytes
   FinishParams begin = fp;
   begin.mode = bsr::kFinishBegin;
@@ -848,7 +878,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   st = bsr_stats{};
   st.request_id = request_id;
   st.n_hit_chunks = n_hit;
-  st.window_chunks = c->W;
+  st.window_chunks = c->W;  // 0: whole-plan mode
   st.install_batch = c->batch;
   st.slot_bytes = c->geo.slot_bytes;
   st.staging_required_bytes = need;
@@ -867,7 +897,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   Session& s = c->s;
   if (!s.active || s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
   if (s.failed) return fail_with(BSR_E_STATE, "request %llu already failed", (unsigned long long)request_id);
-  if (n_chunks == 0 || n_chunks > c->W) return fail_with(BSR_E_ARG, "n_chunks %u must be in 1..W=%u", n_chunks, c->W);
+  if (n_chunks == 0 || n_chunks > s.window) return fail_with(BSR_E_ARG, "n_chunks %u must be in 1..W=%u", n_chunks, s.window);
   if (first_chunk != s.next_chunk) return fail_with(BSR_E_STATE, "window starts at %u, expected %u", first_chunk, s.next_chunk);
   if (static_cast<uint64_t>(first_chunk) + n_chunks > s.n_hit)
     return fail_with(BSR_E_ARG, "window [%u, %u) beyond the bound prefix %u", first_chunk, first_chunk + n_chunks, s.n_hit);
@@ -925,7 +955,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       }
     }
     // the slot must have been released by the install of its previous chunk
-    const uint32_t slot = i % c->W;
+    const uint32_t slot = i % s.window;
     const int64_t need_seq = s.slot_free_seq[slot];
     if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
       if ((rc = hip_check(hipStreamWaitEvent(s.copy, c->free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;

@@ -40,22 +40,37 @@ def status_dict(raw: torch.Tensor) -> dict:
 
 
 class RestoreSession:
+    """One ring (exactly the plan's staging bytes), one status block, two streams.
+
+    With a bounded window the ring is W x chunk bytes and allocated once; in
+    whole-plan mode (W = 0) it is sized per request, n_hit x chunk bytes.
+    """
+
     def __init__(self, ctx: bsr.Ctx, device: str = "cuda:0"):
         self.ctx = ctx
         self.device = torch.device(device)
-        self.staging_bytes = bsr.bsr_staging_bytes(ctx.layout, ctx.window_chunks)
-        self.staging = torch.empty(self.staging_bytes, dtype=torch.uint8, device=self.device)
+        self.staging = None
+        self.staging_bytes = 0
+        if ctx.window_chunks:
+            self._ring(bsr.bsr_plan_staging_bytes(ctx, 0))
         self.status = torch.zeros(64, dtype=torch.uint8, device=self.device)
         self.copy_stream = torch.cuda.Stream(device=self.device)
         self.compute_stream = torch.cuda.Stream(device=self.device)
 
+    def _ring(self, nbytes: int) -> None:
+        if self.staging is None or self.staging.numel() != nbytes:
+            self.staging = None
+            self.staging = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.staging_bytes = nbytes
+
     def bind(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst]) -> None:
+        self._ring(bsr.bsr_plan_staging_bytes(self.ctx, n_hit))
         bsr.bsr_request_bind(self.ctx, request_id, n_hit, dsts, self.staging.data_ptr(),
                              self.staging_bytes, self.status.data_ptr(),
                              self.copy_stream.cuda_stream, self.compute_stream.cuda_stream)
 
     def windows(self, n_hit: int) -> List[Tuple[int, int]]:
-        W = self.ctx.window_chunks
+        W = self.ctx.window_chunks or max(1, n_hit)
         return [(s, min(W, n_hit - s)) for s in range(0, n_hit, W)]
 
     def restore(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst],

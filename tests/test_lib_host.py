@@ -164,11 +164,23 @@ def test_argument_and_state_errors():
         bsr.bsr_slot_bytes(bsr.make_layout(256, [(128, 8, 132, 1, 132)]))   # split == record
     with pytest.raises(bsr.BsrError):
         bsr.bsr_staging_bytes(L, 0)
-    with pytest.raises(bsr.BsrError) as e:
-        bsr.bsr_ctx_create(L, 0, hip_device=-1)
-    assert e.value.code == bsr.BSR_E_ARG
     with pytest.raises(bsr.BsrError):
         bsr.bsr_ctx_create(L, 4, hip_device=-1, install_batch=5)
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(L, 0, hip_device=-1, install_batch=bsr.BSR_MAX_INSTALL_BATCH + 1)
+    assert e.value.code == bsr.BSR_E_ARG
+    # W = 0 is the whole-plan mode: the ring holds the whole plan (Eq. 2)
+    whole = bsr.bsr_ctx_create(L, 0, hip_device=-1)
+    try:
+        assert bsr.bsr_plan_staging_bytes(whole, 2048) == 2048 * 9_707_520
+        assert bsr.bsr_plan_staging_bytes(whole, 7) == 7 * 9_707_520
+    finally:
+        bsr.bsr_ctx_destroy(whole)
+    bounded = bsr.bsr_ctx_create(L, 32, hip_device=-1)
+    try:
+        assert bsr.bsr_plan_staging_bytes(bounded, 2048) == bsr.bsr_plan_staging_bytes(bounded, 3) == 32 * 9_707_520
+    finally:
+        bsr.bsr_ctx_destroy(bounded)
     ctx = bsr.bsr_ctx_create(L, 4, hip_device=-1)
     try:
         with pytest.raises(bsr.BsrError) as e:
