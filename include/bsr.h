@@ -96,6 +96,15 @@ extern "C" {
 #define BSR_INJECT_DELAY_MS 1       /* sleep param ms before fetching chunk */
 #define BSR_INJECT_TRANSFER_ERROR 2 /* treat chunk's copy submission as failed */
 
+/* external tiers, in the probe's order of preference (§4 "System topology":
+ * remote DRAM first, local SSD as the lower reusable tier) */
+#define BSR_TIER_PINNED 0 /* the pinned-host store (bsr_store_*) */
+#define BSR_TIER_FILE 1   /* the file-backed lower tier (bsr_file_tier_*) */
+#define BSR_TIER_NONE 255
+
+/* bsr_file_tier_open flags */
+#define BSR_FILE_DIRECT 1u /* read chunk files with O_DIRECT (bypass the page cache) */
+
 /* struct ids for bsr_struct_size */
 #define BSR_STRUCT_LAYOUT 1
 #define BSR_STRUCT_CONFIG 2
@@ -178,6 +187,9 @@ typedef struct bsr_stats {
   uint64_t commit_wait_ns;         /* host time commit waited for the device */
   double install_ms_total;         /* sum of install-kernel durations (BSR_FLAG_TIME_INSTALL) */
   double install_ms_max;           /* longest install launch (BSR_FLAG_TIME_INSTALL) */
+  uint64_t host_bounce_bytes;      /* pinned host landing zone of the file tier (when it served chunks) */
+  uint32_t file_tier_chunks;       /* chunks restored from the file tier */
+  uint32_t reserved0;
 } bsr_stats;
 
 typedef struct bsr_ctx bsr_ctx;
@@ -261,13 +273,47 @@ int bsr_store_payload(bsr_ctx* ctx, uint64_t key, uint32_t group, void** host_pt
 /* Number of live (key, group) entries and arena bytes in use. */
 int bsr_store_count(bsr_ctx* ctx, uint64_t* n_entries, uint64_t* bytes_used);
 
+/* ---- lower tier: files (§4 "System topology", "Storage-side concurrency is
+ * orthogonal"; §6.4 outcome table; §6.5) ---------------------------------------- */
+
+/* Open (create) a file-backed lower tier in directory `dir`: one file per
+ * chunk key, a 4 KiB header (magic, key, group mask, per-group tags) then
+ * the chunk laid out like a staging slot, padded to 4 KiB.  Files already in
+ * the directory with this layout are indexed (the tier outlives processes).
+ * Restores read chunk files with load_concurrency reader threads (1..64,
+ * the load concurrency of §4) into a pool of readahead_chunks pinned bounce
+ * buffers (0 = 2 x load_concurrency; else >= load_concurrency), each reused
+ * once the device copy out of it has run.  flags: BSR_FILE_DIRECT. */
+int bsr_file_tier_open(bsr_ctx* ctx, const char* dir, uint32_t load_concurrency, uint32_t readahead_chunks,
+                       uint32_t flags);
+
+/* Write the chunk of `key` into the file tier (all groups; tags as for
+ * bsr_store_put_chunk).  Replaces an existing file. */
+int bsr_file_tier_put_chunk(bsr_ctx* ctx, uint64_t key, const void* const* group_payloads);
+
+/* Remove one group's entry (group >= 0) or the whole chunk (group < 0).
+ * BSR_E_NOTFOUND if absent. */
+int bsr_file_tier_remove(bsr_ctx* ctx, uint64_t key, int32_t group);
+
+/* Number of (key, group) entries in the file tier (0 if not open). */
+int bsr_file_tier_count(bsr_ctx* ctx, uint64_t* n_entries);
+
+/* Mark a tier available or not (models a remote store going away).  The
+ * probe skips unavailable tiers; a chunk whose tier became unavailable after
+ * the probe fails its window as missing. */
+int bsr_tier_set_available(bsr_ctx* ctx, int32_t tier, int32_t available);
+
+/* Per-chunk tier chosen by the last probe of `request_id` (BSR_TIER_*; the
+ * first available tier holding every group of the chunk), for n_chunks. */
+int bsr_plan_tiers(bsr_ctx* ctx, uint64_t request_id, uint8_t* tier_of_chunk, uint32_t n_chunks);
+
 /* ---- the hot path ------------------------------------------------------------- */
 
 /* Probe-only lookup (§3 "Probe globally", §4 probe_only).  Computes the
  * chunk keys of `tokens` (see bsr_chunk_keys) and looks every (key, group)
- * up in the store.  hit_bitmap bit i (LSB-first within byte i/8) is 1 iff
- * every group of chunk i is present; *n_hit_chunks is the number of leading
- * ones.  Nothing is staged, no reference is kept, and the store is not
+ * up in the available tiers (the pinned store first, then the file tier).
+ * hit_bitmap bit i (LSB-first within byte i/8) is 1 iff one available tier
+ * holds every group of chunk i; *n_hit_chunks is the number of leading ones.  Nothing is staged, no reference is kept, and the store is not
  * modified.  If the request carries a force-local marker (§3 "Recover
  * without re-entering the same fault") the result is 0 hits and an all-zero
  * bitmap.  The request's plan (keys, n) is kept for bsr_request_bind.

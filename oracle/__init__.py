@@ -24,6 +24,9 @@ Parity status of each part (what pins it, other than itself):
   * probe prefix, windowed restore image, staging accounting, commit rule:
     pinned by the paper's closed forms and printed numbers (Eq. 5 law,
     whole-plan peaks, Prop. 1, Prop. 2, Theta(|S|) installed bytes).
+  * tier choice (remote store, then a lower reusable tier): pinned by the
+    outcome table of §6.4 (full reuse from the lower tier when the remote is
+    unavailable, zero when both are absent).
 """
 
 from .fnv import fnv1a64, fnv0_64, FNV64_OFFSET_BASIS, FNV64_PRIME  # noqa: F401
@@ -31,6 +34,7 @@ from .keys import chunk_digest, chain_keys  # noqa: F401
 from .layout import OracleLayout  # noqa: F401
 from .tag import entry_tag  # noqa: F401
 from .store import OracleStore  # noqa: F401
+from .tiers import Tier, probe_tiers, PlannedStore, NO_TIER  # noqa: F401
 from .restore import (  # noqa: F401
     FAIL_NONE, FAIL_MISSING, FAIL_CORRUPT, FAIL_TIMEOUT, FAIL_TRANSFER, FAIL_ABORT,
     Runtime, RestoreResult, probe, plan_windows, live_trace, peak_live_staging,

@@ -32,6 +32,8 @@ BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT = 3, 4, 5
 BSR_KIND_CONTIG, BSR_KIND_PLANAR = 0, 1
 BSR_FLAG_TIME_INSTALL = 1
 BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR = 0, 1, 2
+BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
+BSR_FILE_DIRECT = 1
 
 _STRUCT_IDS = {"layout": 1, "config": 2, "group_dst": 3, "dev_status": 4, "stats": 5}
 
@@ -74,7 +76,9 @@ class bsr_stats(ct.Structure):
                 ("fallback", ct.c_int32), ("fail_reason", ct.c_int32),
                 ("first_failed_chunk", ct.c_uint32), ("q_mask", ct.c_uint32),
                 ("probe_ns", ct.c_uint64), ("enqueue_ns", ct.c_uint64), ("commit_wait_ns", ct.c_uint64),
-                ("install_ms_total", ct.c_double), ("install_ms_max", ct.c_double)]
+                ("install_ms_total", ct.c_double), ("install_ms_max", ct.c_double),
+                ("host_bounce_bytes", ct.c_uint64), ("file_tier_chunks", ct.c_uint32),
+                ("reserved0", ct.c_uint32)]
 
 
 class BsrError(RuntimeError):
@@ -115,6 +119,12 @@ def _load() -> ct.CDLL:
         "bsr_stats_get": (ct.c_int, [VP, P(bsr_stats)]),
         "bsr_debug_inject": (ct.c_int, [VP, I32, U32, U32]),
         "bsr_measure_h2d": (ct.c_int, [VP, U64, U32, U32, P(ct.c_double)]),
+        "bsr_file_tier_open": (ct.c_int, [VP, ct.c_char_p, U32, U32, U32]),
+        "bsr_file_tier_put_chunk": (ct.c_int, [VP, U64, P(VP)]),
+        "bsr_file_tier_remove": (ct.c_int, [VP, U64, I32]),
+        "bsr_file_tier_count": (ct.c_int, [VP, P(U64)]),
+        "bsr_tier_set_available": (ct.c_int, [VP, I32, I32]),
+        "bsr_plan_tiers": (ct.c_int, [VP, U64, VP, U32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -311,3 +321,35 @@ def bsr_measure_h2d(ctx: Ctx, nbytes: int, n_streams: int = 1, reps: int = 10) -
     g = ct.c_double()
     _check(_lib.bsr_measure_h2d(ctx, nbytes, n_streams, reps, ct.byref(g)))
     return g.value
+
+
+# ---- file-backed lower tier ------------------------------------------------------
+def bsr_file_tier_open(ctx: Ctx, directory: str, load_concurrency: int = 1, readahead_chunks: int = 0,
+                       flags: int = 0) -> None:
+    _check(_lib.bsr_file_tier_open(ctx, directory.encode(), load_concurrency, readahead_chunks, flags))
+
+
+def bsr_file_tier_put_chunk(ctx: Ctx, key: int, payloads: Sequence[np.ndarray]) -> None:
+    arrs = [np.ascontiguousarray(p, dtype=np.uint8) for p in payloads]
+    ptrs = (ct.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
+    _check(_lib.bsr_file_tier_put_chunk(ctx, int(key), ptrs))
+
+
+def bsr_file_tier_remove(ctx: Ctx, key: int, group: int = -1) -> None:
+    _check(_lib.bsr_file_tier_remove(ctx, int(key), group))
+
+
+def bsr_file_tier_count(ctx: Ctx) -> int:
+    n = ct.c_uint64()
+    _check(_lib.bsr_file_tier_count(ctx, ct.byref(n)))
+    return n.value
+
+
+def bsr_tier_set_available(ctx: Ctx, tier: int, available: bool) -> None:
+    _check(_lib.bsr_tier_set_available(ctx, tier, int(bool(available))))
+
+
+def bsr_plan_tiers(ctx: Ctx, request_id: int, n_chunks: int) -> np.ndarray:
+    out = np.zeros(max(1, n_chunks), dtype=np.uint8)
+    _check(_lib.bsr_plan_tiers(ctx, request_id, _ptr(out), n_chunks))
+    return out[:n_chunks]

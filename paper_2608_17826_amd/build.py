@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libbsr.so")
 
-SOURCES = ["bsr_kernels.hip", "bsr_runtime.cpp"]
+SOURCES = ["bsr_kernels.hip", "bsr_runtime.cpp", "bsr_file_tier.cpp"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", "-Wall",

@@ -32,6 +32,7 @@
 
 #include "bsr.h"
 #include "bsr_device.h"
+#include "bsr_file_tier.h"
 
 namespace {
 
@@ -293,8 +294,13 @@ struct Store {
 // ---------------------------------------------------------------------------
 enum class Phase { Probed, Bound, Failed, Done };
 
+constexpr uint8_t kTierPinned = 0;  // the pinned-host store
+constexpr uint8_t kTierFile = 1;    // the file-backed lower tier
+constexpr uint8_t kTierNone = 0xFF;
+
 struct Request {
   std::vector<uint64_t> keys;
+  std::vector<uint8_t> tier;  // per chunk: the tier the probe found it in
   uint32_t n_probe = 0;
   Phase phase = Phase::Probed;
 };
@@ -342,6 +348,8 @@ struct bsr_ctx {
   Store store;
   std::unordered_map<uint64_t, Request> requests;
   std::unordered_set<uint64_t> force_local;
+  bool tier0_available = true;
+  bsr::FileTier ftier;
   Session s;
   bsr_stats stats{};
   Inject inject;
@@ -445,6 +453,7 @@ int enqueue_finish(bsr_ctx* c, uint32_t mode, uint32_t reason, uint32_t chunk, u
 int host_fail(bsr_ctx* c, int reason, uint32_t chunk, uint32_t mask, int code) {
   Session& s = c->s;
   const std::string msg = g_err;
+  c->ftier.drain();  // no read of this request may still target a bounce buffer
   int rc = enqueue_finish(c, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), chunk, mask);
   s.failed = true;
   if (s.host_fail == BSR_FAIL_NONE) s.host_fail = reason;
@@ -579,6 +588,7 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
 
 int bsr_ctx_destroy(bsr_ctx* c) {
   if (!c) return BSR_OK;
+  c->ftier.close();
   if (c->device >= 0) {
     (void)hipSetDevice(c->device);
     if (c->s.active) {
@@ -740,9 +750,19 @@ int bsr_probe(bsr_ctx* c, uint64_t request_id, uint64_t salt, const int32_t* tok
     const bool local = c->force_local.count(request_id) != 0;
     bool prefix = true;
     const uint32_t G = c->geo.L.n_groups;
+    req.tier.assign(N, kTierNone);
+    const bool file_up = c->ftier.is_open() && c->ftier.available;
     for (uint64_t i = 0; i < N && !local; ++i) {
-      bool hit = true;
+      // a chunk is a hit in the first available tier holding every group
+      bool hit = c->tier0_available;
       for (uint32_t g = 0; g < G && hit; ++g) hit = c->store.index[g].count(req.keys[i]) != 0;
+      if (hit) {
+        req.tier[i] = kTierPinned;
+      } else if (file_up) {
+        hit = true;
+        for (uint32_t g = 0; g < G && hit; ++g) hit = c->ftier.has(req.keys[i], g);
+        if (hit) req.tier[i] = kTierFile;
+      }
       if (hit && hit_bitmap) hit_bitmap[i >> 3] |= static_cast<uint8_t>(1u << (i & 7));
       if (!hit) prefix = false;
       if (prefix) ++n_hit;
@@ -915,12 +935,29 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   const uint64_t t_window = now_ns();
   int rc = BSR_OK;
 
+  // Chunks the probe found only in the file tier are read ahead by the
+  // tier's readers into its bounce buffers (at most pool_size in flight) and
+  // consumed in chunk order; each buffer is reused once the device copy out
+  // of it has completed.
+  std::vector<uint32_t> fchunks;
+  for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i)
+    if (rq.tier[i] == kTierFile) fchunks.push_back(i);
+  size_t f_sub = 0, f_used = 0;
+  uint32_t P = 0;
+  if (!fchunks.empty()) {
+    std::string err;
+    if (!c->ftier.is_open()) return fail_with(BSR_E_STATE, "the plan uses the file tier, which is closed");
+    if (c->ftier.start(c->device, &err)) return fail_with(BSR_E_NOMEM, "%s", err.c_str());
+    P = c->ftier.pool_size();
+    for (; f_sub < fchunks.size() && f_sub < P; ++f_sub) c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
+  }
+  const uint64_t deadline = c->cfg.window_timeout_ms ? t_window + static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull : 0;
+
   for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {
     // injected host faults (forced from the host; kernels always exit normally)
     if (c->inject.kind == BSR_INJECT_DELAY_MS && c->inject.chunk == i)
       std::this_thread::sleep_for(std::chrono::milliseconds(c->inject.param));
-    if (c->cfg.window_timeout_ms &&
-        (now_ns() - t_window) > static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull) {
+    if (deadline && now_ns() > deadline) {
       if ((rc = flush_batch(c, batch, tags))) return rc;
       fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded at chunk %u", c->cfg.window_timeout_ms, i);
       return host_fail(c, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
@@ -930,29 +967,63 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       fail_with(BSR_E_TRANSFER, "injected transfer error at chunk %u", i);
       return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
     }
-    // fetch: every group's entry must be present
     const uint64_t key = rq.keys[i];
-    uint32_t missing = 0;
+    const bool from_file = rq.tier[i] == kTierFile;
+    std::array<uint64_t, BSR_MAX_GROUPS> tg{};
+    const uint8_t* src_block = nullptr;  // one contiguous slot-shaped source
     Entry ent[BSR_MAX_GROUPS];
-    for (uint32_t g = 0; g < G; ++g) {
-      auto it = c->store.index[g].find(key);
-      if (it == c->store.index[g].end())
-        missing |= 1u << g;
-      else
-        ent[g] = it->second;
+    bool one_block = true;
+    // fetch: every group's entry must still be present in the chunk's tier
+    uint32_t missing = 0;
+    if (!from_file) {
+      for (uint32_t g = 0; g < G; ++g) {
+        auto it = c->store.index[g].find(key);
+        if (!c->tier0_available || it == c->store.index[g].end())
+          missing |= 1u << g;
+        else
+          ent[g] = it->second;
+      }
+    } else {
+      for (uint32_t g = 0; g < G; ++g)
+        if (!c->ftier.available || !c->ftier.tag(key, g, &tg[g])) missing |= 1u << g;
     }
     if (missing) {
       if ((rc = flush_batch(c, batch, tags))) return rc;
       fail_with(BSR_E_MISSING, "chunk %u: entries missing for group mask 0x%x", i, missing);
       return host_fail(c, BSR_FAIL_MISSING, i, missing, BSR_E_MISSING);
     }
-    bool one_block = true;
-    for (uint32_t g = 1; g < G; ++g) one_block = one_block && ent[g].block == ent[0].block;
-    for (uint32_t g = 0; g < G; ++g) {
-      if (g == 0 || !one_block) {
-        ++c->store.meta[ent[g].block].refs;
-        s.refs.push_back(ent[g].block);
+    uint32_t bounce = 0;
+    if (from_file) {
+      // wait for the chunk's read (complete presence of the object)
+      bounce = static_cast<uint32_t>(f_used % P);
+      uint32_t present = 0;
+      int os_err = 0;
+      const int st = c->ftier.wait(bounce, deadline, &present, &os_err);
+      if (st != bsr::FileTier::kReadOk || (present & all_mask) != all_mask) {
+        if ((rc = flush_batch(c, batch, tags))) return rc;
+        if (st == bsr::FileTier::kReadPending) {
+          fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded reading chunk %u", c->cfg.window_timeout_ms, i);
+          return host_fail(c, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
+        }
+        if (st == bsr::FileTier::kReadIoError) {
+          fail_with(BSR_E_TRANSFER, "chunk %u: file read failed: %s", i, std::strerror(os_err));
+          return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+        }
+        const uint32_t miss = st == bsr::FileTier::kReadOk ? (all_mask & ~present) : all_mask;
+        fail_with(BSR_E_MISSING, "chunk %u: file entry missing for group mask 0x%x", i, miss);
+        return host_fail(c, BSR_FAIL_MISSING, i, miss, BSR_E_MISSING);
       }
+      src_block = c->ftier.bounce_data(bounce);
+    } else {
+      for (uint32_t g = 1; g < G; ++g) one_block = one_block && ent[g].block == ent[0].block;
+      for (uint32_t g = 0; g < G; ++g) {
+        tg[g] = ent[g].tag;
+        if (g == 0 || !one_block) {
+          ++c->store.meta[ent[g].block].refs;
+          s.refs.push_back(ent[g].block);
+        }
+      }
+      if (one_block) src_block = c->store.block_ptr(ent[0].block);
     }
     // the slot must have been released by the install of its previous chunk
     const uint32_t slot = i % s.window;
@@ -963,12 +1034,22 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     }
     uint8_t* dst = s.staging + static_cast<uint64_t>(slot) * c->geo.slot_bytes;
     hipError_t e = hipSuccess;
-    if (one_block) {
-      e = hipMemcpyAsync(dst, c->store.block_ptr(ent[0].block), c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
+    if (src_block) {
+      e = hipMemcpyAsync(dst, src_block, c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
     } else {
       for (uint32_t g = 0; g < G && e == hipSuccess; ++g)
         e = hipMemcpyAsync(dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
                            c->geo.payload[g], hipMemcpyHostToDevice, s.copy);
+    }
+    if (e == hipSuccess && from_file) {
+      // the bounce buffer is free again once this copy has run
+      e = hipEventRecord(c->ftier.bounce_event(bounce), s.copy);
+      ++f_used;
+      if (e == hipSuccess && f_sub < fchunks.size()) {
+        c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
+        ++f_sub;
+      }
+      ++c->stats.file_tier_chunks;
     }
     if (e != hipSuccess) {
       const std::string why = hipGetErrorString(e);
@@ -981,8 +1062,6 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       s.slot_used[slot] = 1;
       ++s.slots_touched;
     }
-    std::array<uint64_t, BSR_MAX_GROUPS> tg{};
-    for (uint32_t g = 0; g < G; ++g) tg[g] = ent[g].tag;
     batch.push_back(i);
     tags.push_back(tg);
     ++c->stats.n_chunks_enqueued;
@@ -994,6 +1073,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   s.next_chunk = first_chunk + n_chunks;
   ++c->stats.n_windows;
   c->stats.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
+  if (!fchunks.empty()) c->stats.host_bounce_bytes = c->ftier.bounce_bytes();
   c->stats.enqueue_ns += now_ns() - t_enter;
   return BSR_OK;
 }
@@ -1032,6 +1112,7 @@ static int complete_session(bsr_ctx* c, bool run_commit, uint64_t* exposed, int3
     if (!rc) rc = enqueue_finish(c, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
   }
   if (!rc) rc = flush_batch(c, s.pend, s.pend_tags);
+  c->ftier.drain();
   const uint64_t t0 = now_ns();
   if (!rc) rc = hip_check(hipMemcpyAsync(c->host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
   int rc2 = hip_check(hipStreamSynchronize(s.compute), "hipStreamSynchronize(compute)");
@@ -1103,6 +1184,76 @@ int bsr_request_end(bsr_ctx* c, uint64_t request_id) {
   c->force_local.erase(request_id);
   c->requests.erase(request_id);
   return rc;
+}
+
+// ---- file-backed lower tier ----------------------------------------------------
+
+int bsr_file_tier_open(bsr_ctx* c, const char* dir, uint32_t load_concurrency, uint32_t readahead_chunks,
+                       uint32_t flags) {
+  if (!c || !dir) return fail_with(BSR_E_ARG, "ctx or dir is NULL");
+  if (load_concurrency == 0 || load_concurrency > 64) return fail_with(BSR_E_ARG, "load_concurrency must be 1..64");
+  if (readahead_chunks && readahead_chunks < load_concurrency)
+    return fail_with(BSR_E_ARG, "readahead_chunks must be 0 or >= load_concurrency");
+  if (flags & ~BSR_FILE_DIRECT) return fail_with(BSR_E_ARG, "unknown flags 0x%x", flags);
+  std::lock_guard<std::mutex> lk(c->mu);
+  std::string err;
+  if (c->ftier.open(dir, c->geo.L.n_groups, c->geo.slot_bytes, c->geo.offset, c->geo.payload, load_concurrency,
+                    readahead_chunks, (flags & BSR_FILE_DIRECT) != 0, &err))
+    return fail_with(BSR_E_ARG, "%s", err.c_str());
+  return BSR_OK;
+}
+
+int bsr_file_tier_put_chunk(bsr_ctx* c, uint64_t key, const void* const* payloads) {
+  if (!c || !payloads) return fail_with(BSR_E_ARG, "ctx or payloads is NULL");
+  if (!c->ftier.is_open()) return fail_with(BSR_E_STATE, "file tier is not open");
+  const uint32_t G = c->geo.L.n_groups;
+  uint64_t tags[BSR_MAX_GROUPS] = {};
+  for (uint32_t g = 0; g < G; ++g) {
+    if (!payloads[g]) return fail_with(BSR_E_ARG, "payload of group %u is NULL", g);
+    tags[g] = tag_of(static_cast<const uint8_t*>(payloads[g]), c->geo.payload[g]);
+  }
+  std::string err;
+  if (c->ftier.put(key, payloads, tags, &err)) return fail_with(BSR_E_TRANSFER, "%s", err.c_str());
+  return BSR_OK;
+}
+
+int bsr_file_tier_remove(bsr_ctx* c, uint64_t key, int32_t group) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (!c->ftier.is_open()) return fail_with(BSR_E_STATE, "file tier is not open");
+  if (group >= static_cast<int32_t>(c->geo.L.n_groups)) return fail_with(BSR_E_ARG, "group %d out of range", group);
+  std::string err;
+  const int r = c->ftier.remove(key, group, &err);
+  if (r > 0) return fail_with(BSR_E_NOTFOUND, "%s", err.c_str());
+  if (r < 0) return fail_with(BSR_E_TRANSFER, "%s", err.c_str());
+  return BSR_OK;
+}
+
+int bsr_file_tier_count(bsr_ctx* c, uint64_t* n_entries) {
+  if (!c || !n_entries) return fail_with(BSR_E_ARG, "ctx or out is NULL");
+  *n_entries = c->ftier.is_open() ? c->ftier.n_entries() : 0;
+  return BSR_OK;
+}
+
+int bsr_tier_set_available(bsr_ctx* c, int32_t tier, int32_t available) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (tier == BSR_TIER_PINNED)
+    c->tier0_available = available != 0;
+  else if (tier == BSR_TIER_FILE)
+    c->ftier.available = available != 0;
+  else
+    return fail_with(BSR_E_ARG, "unknown tier %d", tier);
+  return BSR_OK;
+}
+
+int bsr_plan_tiers(bsr_ctx* c, uint64_t request_id, uint8_t* tier_of_chunk, uint32_t n_chunks) {
+  if (!c || !tier_of_chunk) return fail_with(BSR_E_ARG, "ctx or out is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  auto it = c->requests.find(request_id);
+  if (it == c->requests.end()) return fail_with(BSR_E_NOTFOUND, "request %llu was not probed", (unsigned long long)request_id);
+  const auto& t = it->second.tier;
+  for (uint32_t i = 0; i < n_chunks; ++i) tier_of_chunk[i] = i < t.size() ? t[i] : kTierNone;
+  return BSR_OK;
 }
 
 int bsr_stats_get(bsr_ctx* c, bsr_stats* out) {

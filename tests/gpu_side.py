@@ -33,31 +33,44 @@ class GpuCase:
     """Library context + pinned store holding the workload's chunks + device pools."""
 
     def __init__(self, wi: WorkloadInputs, W: int, install_batch: int = 0, flags: int = 0,
-                 timeout_ms: int = 0, held: Optional[int] = None, device: str = "cuda:0"):
+                 timeout_ms: int = 0, held: Optional[int] = None, device: str = "cuda:0",
+                 pinned_chunks=None):
         self.wi = wi
         w = wi.workload
         self.layout = layout_of(wi)
         self.ctx = bsr.bsr_ctx_create(self.layout, W, hip_device=0, install_batch=install_batch,
                                       flags=flags, window_timeout_ms=timeout_ms)
         held = w.held_chunks if held is None else held
+        chunks = list(range(held)) if pinned_chunks is None else list(pinned_chunks)
         slot = bsr.bsr_slot_bytes(self.layout)
         stride = (slot + 4095) // 4096 * 4096
-        bsr.bsr_store_reserve(self.ctx, stride * (held + 2))
+        bsr.bsr_store_reserve(self.ctx, stride * (len(chunks) + 2))
         self.keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
-        self._put(held)
+        self._put(chunks)
         self.dev = place(wi, device)
         torch.cuda.synchronize()
         self.session = RestoreSession(self.ctx, device)
 
-    def _put(self, held: int) -> None:
+    def _put(self, chunks) -> None:
         def put(i):
             bsr.bsr_store_put_chunk(self.ctx, int(self.keys[i]), self.wi.payloads(i))
-        if held > 64:
+        if len(chunks) > 64:
             with ThreadPoolExecutor(8) as ex:
-                list(ex.map(put, range(held)))
+                list(ex.map(put, chunks))
         else:
-            for i in range(held):
+            for i in chunks:
                 put(i)
+
+    def put_files(self, directory: str, chunks, concurrency: int = 2, readahead: int = 0,
+                  direct: bool = False) -> None:
+        """Open the file-backed lower tier and write the given chunks to it."""
+        bsr.bsr_file_tier_open(self.ctx, directory, concurrency, readahead,
+                               bsr.BSR_FILE_DIRECT if direct else 0)
+
+        def put(i):
+            bsr.bsr_file_tier_put_chunk(self.ctx, int(self.keys[i]), self.wi.payloads(i))
+        with ThreadPoolExecutor(8) as ex:
+            list(ex.map(put, list(chunks)))
 
     def dsts(self):
         return group_dsts(self.dev.block_tables, self.dev.tensor_bases, self.dev.valid, self.wi.pool_blocks)

@@ -1,0 +1,95 @@
+"""Host-side checks of the file-backed lower tier (CPU, host-only context)."""
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle_side import build_case
+from paper_2608_17826_amd import bsr
+from workloads import generate, get_config
+from workloads.gen import random_workload
+
+KIND = {"contig": bsr.BSR_KIND_CONTIG, "planar": bsr.BSR_KIND_PLANAR}
+
+
+def _layout(w):
+    return bsr.make_layout(w.chunk_tokens, [(s.block_tokens, s.n_tensors, s.record_bytes, KIND[s.kind],
+                                             s.split_bytes) for s in w.groups])
+
+
+def _ctx(w, tmp_path, arena_chunks):
+    ctx = bsr.bsr_ctx_create(_layout(w), 2, hip_device=-1)
+    slot = bsr.bsr_slot_bytes(ctx.layout)
+    arena = np.zeros(((slot + 4095) // 4096 * 4096) * (arena_chunks + 1), np.uint8)
+    bsr.bsr_store_adopt(ctx, arena.ctypes.data, arena.nbytes)
+    bsr.bsr_file_tier_open(ctx, str(tmp_path), 2)
+    return ctx, arena
+
+
+def test_file_tier_put_reopen_remove(tmp_path):
+    w = random_workload(5)
+    wi = generate(w)
+    case = build_case(wi, with_pools=False)
+    G = len(w.groups)
+    ctx, arena = _ctx(w, tmp_path, 1)
+    try:
+        for i in range(w.held_chunks):
+            bsr.bsr_file_tier_put_chunk(ctx, case.keys[i], wi.payloads(i))
+        assert bsr.bsr_file_tier_count(ctx) == w.held_chunks * G
+        files = sorted(os.listdir(tmp_path))
+        assert len(files) == w.held_chunks and all(f.endswith(".bsr") for f in files)
+        size = os.path.getsize(tmp_path / files[0])
+        slot = bsr.bsr_slot_bytes(ctx.layout)
+        assert size == 4096 + (slot + 4095) // 4096 * 4096
+        bsr.bsr_file_tier_remove(ctx, case.keys[0], G - 1)
+        assert bsr.bsr_file_tier_count(ctx) == w.held_chunks * G - 1
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_file_tier_remove(ctx, case.keys[0], G - 1)
+        assert e.value.code == bsr.BSR_E_NOTFOUND
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
+    # a new context re-indexes the directory, including the removed group
+    ctx2, arena2 = _ctx(w, tmp_path, 1)
+    try:
+        assert bsr.bsr_file_tier_count(ctx2) == w.held_chunks * G - 1
+        n, bm, _ = bsr.bsr_probe(ctx2, 1, wi.salt, wi.tokens)
+        assert n == 0 and bm[1:].all() and not bm[0]
+        bsr.bsr_file_tier_remove(ctx2, case.keys[0])      # whole chunk: the file goes
+        assert len(os.listdir(tmp_path)) == w.held_chunks - 1
+    finally:
+        bsr.bsr_ctx_destroy(ctx2)
+
+
+def test_probe_tier_choice_matches_oracle(tmp_path):
+    wi = generate(get_config(1))
+    case = build_case(wi, with_pools=False)
+    ctx, arena = _ctx(wi.workload, tmp_path, 16)
+    remote, ssd = oracle.OracleStore(1), oracle.OracleStore(1)
+    try:
+        for i in range(0, 10):
+            bsr.bsr_store_put_chunk(ctx, case.keys[i], wi.payloads(i))
+            remote.put_chunk(case.keys[i], wi.payloads(i))
+        for i in range(6, 16):
+            bsr.bsr_file_tier_put_chunk(ctx, case.keys[i], wi.payloads(i))
+            ssd.put_chunk(case.keys[i], wi.payloads(i))
+        tiers = [oracle.Tier(remote), oracle.Tier(ssd)]
+        for avail in [(1, 1), (0, 1), (1, 0), (0, 0)]:
+            bsr.bsr_tier_set_available(ctx, bsr.BSR_TIER_PINNED, avail[0])
+            bsr.bsr_tier_set_available(ctx, bsr.BSR_TIER_FILE, avail[1])
+            tiers[0].available, tiers[1].available = bool(avail[0]), bool(avail[1])
+            rid = 10 + avail[0] * 2 + avail[1]
+            n, bm, _ = bsr.bsr_probe(ctx, rid, wi.salt, wi.tokens)
+            on, obm, _, oct_ = oracle.probe_tiers(tiers, wi.tokens, 64, wi.salt, 1)
+            assert n == on, avail
+            np.testing.assert_array_equal(bm, obm)
+            np.testing.assert_array_equal(bsr.bsr_plan_tiers(ctx, rid, 16), oct_)
+        # both available: remote first, the lower tier extends the prefix
+        assert bsr.bsr_probe(ctx, 99, wi.salt, wi.tokens)[0] == 0  # both unavailable from the loop end
+        bsr.bsr_tier_set_available(ctx, bsr.BSR_TIER_PINNED, 1)
+        bsr.bsr_tier_set_available(ctx, bsr.BSR_TIER_FILE, 1)
+        assert bsr.bsr_probe(ctx, 100, wi.salt, wi.tokens)[0] == 16
+        assert list(bsr.bsr_plan_tiers(ctx, 100, 16)) == [0] * 10 + [1] * 6
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
