@@ -43,6 +43,13 @@ def parse():
                     help="also run a plain 1 GiB device copy (for counter calibration)")
     ap.add_argument("--held-chunks", type=int, default=0,
                     help="profiling passes only: hold just the first N chunks (same launch shape)")
+    ap.add_argument("--tier", choices=["pinned", "file"], default="pinned",
+                    help="external tier holding the chunks: the pinned-host store or the file tier")
+    ap.add_argument("--file-dir", default="", help="file tier directory (default /tmp/bsr_tier_<workload>)")
+    ap.add_argument("--load-concurrency", type=int, default=4, help="file tier reader threads")
+    ap.add_argument("--direct", action="store_true", help="file tier reads with O_DIRECT")
+    ap.add_argument("--concurrency-sweep", default="",
+                    help="file tier only: comma-separated load concurrencies to measure as well")
     return ap.parse_args()
 
 
@@ -73,17 +80,25 @@ def main():
     slot = bsr.bsr_slot_bytes(layout)
     stride = (slot + 4095) // 4096 * 4096
     held = w.held_chunks if not args.held_chunks else min(args.held_chunks, w.held_chunks)
-    log(f"[bench] pinned store: {held} chunks x {slot} B")
-    bsr.bsr_store_reserve(ctx, stride * (held + 1))
     keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
-
-    def put(i):
-        bsr.bsr_store_put_chunk(ctx, int(keys[i]), wi.payloads(i))
-
+    file_dir = args.file_dir or f"/tmp/bsr_tier_{w.name}"
     t0 = time.time()
+    if args.tier == "pinned":
+        log(f"[bench] pinned store: {held} chunks x {slot} B")
+        bsr.bsr_store_reserve(ctx, stride * (held + 1))
+
+        def put(i):
+            bsr.bsr_store_put_chunk(ctx, int(keys[i]), wi.payloads(i))
+    else:
+        log(f"[bench] file tier {file_dir}: {held} chunks x {slot} B, load concurrency {args.load_concurrency}")
+        bsr.bsr_store_reserve(ctx, stride)
+        open_file_tier(bsr, ctx, file_dir, args.load_concurrency, args.direct)
+
+        def put(i):
+            bsr.bsr_file_tier_put_chunk(ctx, int(keys[i]), wi.payloads(i))
     with ThreadPoolExecutor(8) as ex:
         list(ex.map(put, range(held)))
-    log(f"[bench] store filled in {time.time() - t0:.1f}s")
+    log(f"[bench] tier filled in {time.time() - t0:.1f}s")
     dev = place(wi)
     torch.cuda.synchronize()
     dsts = group_dsts(dev.block_tables, dev.tensor_bases, dev.valid, wi.pool_blocks)
@@ -142,6 +157,35 @@ def main():
 
     traffic, traffic_src = recorded_traffic(w.name, st["install_batch"])
 
+    sweep = None
+    if args.concurrency_sweep and args.tier == "file":
+        sweep = []
+        for conc in [int(x) for x in args.concurrency_sweep.split(",")]:
+            c2 = bsr.bsr_ctx_create(layout, W, hip_device=0, install_batch=args.install_batch)
+            bsr.bsr_store_reserve(c2, stride)
+            open_file_tier(bsr, c2, file_dir, conc, args.direct)   # re-indexes the same files
+            s2 = RestoreSession(c2)
+            times, outs2 = [], []
+            for i in range(args.warmup + args.steps):
+                n2, _, _ = bsr.bsr_probe(c2, 3000 + i, wi.salt, wi.tokens)
+                t_a = time.perf_counter()
+                o2 = s2.restore(3000 + i, n2, dsts)
+                t_b = time.perf_counter()
+                bsr.bsr_request_end(c2, 3000 + i)
+                assert o2.fallback == 0 and o2.exposed_tokens == n2 * w.chunk_tokens
+                if i >= args.warmup:
+                    times.append(t_b - t_a)
+                    outs2.append(o2)
+            sweep.append({"load_concurrency": conc,
+                          "gbps": round(n2 * chunk_payload * len(times) / sum(times) / 1e9, 3),
+                          "ms_per_restore": round(sum(times) / len(times) * 1e3, 1),
+                          "peak_live_staging_bytes": outs2[-1].stats["peak_live_staging_bytes"],
+                          "host_bounce_bytes": outs2[-1].stats["host_bounce_bytes"],
+                          "file_tier_chunks": outs2[-1].stats["file_tier_chunks"]})
+            log(f"[bench] load concurrency {conc}: {sweep[-1]}")
+            del s2
+            bsr.bsr_ctx_destroy(c2)
+
     cpu = None
     if not args.no_cpu_baseline and W > 0:
         cpu = cpu_baseline(wi, W, args.cpu_seconds)
@@ -189,8 +233,18 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if args.tier == "file":
+        line["file_tier"] = {"dir": file_dir, "direct": bool(args.direct),
+                             "load_concurrency": args.load_concurrency,
+                             "host_bounce_bytes": st["host_bounce_bytes"],
+                             "file_tier_chunks": st["file_tier_chunks"],
+                             "concurrency_sweep": sweep}
     print(json.dumps(line), flush=True)
     bsr.bsr_ctx_destroy(ctx)
+
+
+def open_file_tier(bsr, ctx, directory, concurrency, direct):
+    bsr.bsr_file_tier_open(ctx, directory, concurrency, 0, bsr.BSR_FILE_DIRECT if direct else 0)
 
 
 def kernel_sources_sha256():
