@@ -27,6 +27,11 @@ Parity status of each part (what pins it, other than itself):
   * tier choice (remote store, then a lower reusable tier): pinned by the
     outcome table of §6.4 (full reuse from the lower tier when the remote is
     unavailable, zero when both are absent).
+  * global admission budget B (§7): pinned by closed forms (B = 0 is the
+    one-at-a-time lock; with a bounded window the number admitted together
+    is floor(B / (W c)) whatever the plan lengths, Prop. 1) and by brute
+    force over short event sequences (the aggregate never exceeds B, and
+    every refusal is forced by B or by the slot count).
 """
 
 from .fnv import fnv1a64, fnv0_64, FNV64_OFFSET_BASIS, FNV64_PRIME  # noqa: F401
@@ -35,6 +40,7 @@ from .layout import OracleLayout  # noqa: F401
 from .tag import entry_tag  # noqa: F401
 from .store import OracleStore  # noqa: F401
 from .tiers import Tier, probe_tiers, PlannedStore, NO_TIER  # noqa: F401
+from . import admission  # noqa: F401
 from .restore import (  # noqa: F401
     FAIL_NONE, FAIL_MISSING, FAIL_CORRUPT, FAIL_TIMEOUT, FAIL_TRANSFER, FAIL_ABORT,
     Runtime, RestoreResult, probe, plan_windows, live_trace, peak_live_staging,
