@@ -23,10 +23,12 @@
  *     HIP device pointers on the context's device; all others are host
  *     pointers.  Streams are hipStream_t handles passed as void*.
  *   - Sizes are in bytes unless named *_tokens, *_chunks or *_blocks.
- *   - One context serves one GPU rank.  Store and probe calls are thread
- *     safe; one request at a time may be bound (the bounded-retrieve lock of
- *     §3 "Install locally"), and the calls for the bound request must come
- *     from one thread at a time.
+ *   - One context serves one GPU rank.  Every call is thread safe (calls on
+ *     one context are serialised by its mutex; device work of different
+ *     requests overlaps on their streams).  By default one request at a time
+ *     may be bound (the bounded-retrieve lock of §3 "Install locally");
+ *     a global admission budget B (bsr_config.staging_budget_bytes, §7) lets
+ *     several be bound while their staging rings together stay within B.
  *
  * Data layout
  *   A chunk is chunk_tokens consecutive tokens.  A group is one allocator
@@ -57,9 +59,10 @@
 extern "C" {
 #endif
 
-#define BSR_ABI_VERSION 1
+#define BSR_ABI_VERSION 2
 #define BSR_MAX_GROUPS 8
 #define BSR_MAX_INSTALL_BATCH 32
+#define BSR_MAX_BOUND_REQUESTS 16 /* session slots of one context */
 #define BSR_NO_CHUNK 0xFFFFFFFFu
 
 /* status codes */
@@ -71,8 +74,8 @@ extern "C" {
 #define BSR_E_TIMEOUT (-5)   /* the window's fetch exceeded its deadline */
 #define BSR_E_TRANSFER (-6)  /* a HIP transfer or launch failed */
 #define BSR_E_NOMEM (-7)     /* store arena full or host/device allocation failed */
-#define BSR_E_STAGING (-8)   /* staging buffer smaller than W * slot bytes */
-#define BSR_E_BUSY (-9)      /* another request holds the bounded-retrieve lock */
+#define BSR_E_STAGING (-8)   /* staging buffer smaller than W * slot bytes, or a ring larger than B */
+#define BSR_E_BUSY (-9)      /* no admission now: the lock is held, B is used up or no session slot is free */
 #define BSR_E_DEVICE (-10)   /* operation needs a GPU context */
 #define BSR_E_NOTFOUND (-11) /* unknown key or request */
 
@@ -111,6 +114,7 @@ extern "C" {
 #define BSR_STRUCT_GROUP_DST 3
 #define BSR_STRUCT_DEV_STATUS 4
 #define BSR_STRUCT_STATS 5
+#define BSR_STRUCT_ADMISSION 6
 
 typedef struct bsr_group_desc {
   uint32_t block_tokens; /* tokens per destination block, >= 1 */
@@ -136,7 +140,18 @@ typedef struct bsr_config {
   int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
   uint32_t flags;             /* BSR_FLAG_* */
   uint32_t window_timeout_ms; /* per-window fetch deadline, 0 = none */
-  uint32_t reserved[3];       /* must be 0 */
+  uint32_t max_bound_requests;   /* session slots: requests that may be bound at once, each with its own
+                                    pre-allocated tag partials, verify words, events and status mirror.
+                                    0 = automatic: 1 when staging_budget_bytes is 0, else
+                                    min(BSR_MAX_BOUND_REQUESTS, B / (max(W, 1) * slot bytes)), i.e. as
+                                    many as B can hold; <= BSR_MAX_BOUND_REQUESTS, and <= 1 when
+                                    staging_budget_bytes is 0 */
+  uint64_t staging_budget_bytes; /* B, the global admission budget (§7 "Current concurrency is
+                                    conservative"): 0 keeps the bounded-retrieve lock (one bound request
+                                    at a time, §3 "Install locally").  B > 0 admits a bind while the
+                                    rings of every bound request plus its own
+                                    (bsr_plan_staging_bytes each) stay <= B; with a bounded window B must
+                                    hold at least one ring */
 } bsr_config;
 
 /* Destination of one group for one request (all pointers device, caller-owned). */
@@ -162,7 +177,7 @@ typedef struct bsr_dev_status {
   uint32_t reserved[2];
 } bsr_dev_status;
 
-/* Host-side counters of the most recent (or current) bound request. */
+/* Host-side counters of one request (bsr_stats_get, bsr_request_stats). */
 typedef struct bsr_stats {
   uint64_t request_id;
   uint32_t n_hit_chunks;        /* n: prefix length bound for restore */
@@ -174,7 +189,8 @@ typedef struct bsr_stats {
   uint64_t slot_bytes;             /* c: bytes of one staged chunk */
   uint64_t staging_required_bytes; /* W * slot_bytes: the ring the caller provides */
   uint64_t peak_live_staging_bytes;/* max slots holding an unreleased chunk, times slot_bytes */
-  uint64_t aux_device_bytes;       /* library-owned device memory, O(W) (Eq. 4 M_aux) */
+  uint64_t aux_device_bytes;       /* library-owned device memory of the request's session slot, O(W)
+                                      (Eq. 4 M_aux) */
   uint64_t h2d_bytes;              /* bytes enqueued host -> device */
   uint64_t installed_bytes;        /* payload bytes enqueued for installation */
   uint64_t exposed_tokens;         /* from the last commit */
@@ -191,6 +207,18 @@ typedef struct bsr_stats {
   uint32_t file_tier_chunks;       /* chunks restored from the file tier */
   uint32_t reserved0;
 } bsr_stats;
+
+/* Admission state of a context (the lock or the global budget B). */
+typedef struct bsr_admission {
+  uint64_t staging_budget_bytes;     /* B as configured (0 = the bounded-retrieve lock) */
+  uint32_t max_bound_requests;       /* session slots */
+  uint32_t n_bound;                  /* requests bound now */
+  uint64_t bound_staging_bytes;      /* sum of the rings of the bound requests */
+  uint64_t peak_bound_staging_bytes; /* its maximum since the context was created */
+  uint32_t peak_n_bound;             /* most requests bound at once */
+  uint32_t n_refused;                /* binds refused with BSR_E_BUSY */
+  uint64_t aux_device_bytes;         /* library-owned device memory of all session slots */
+} bsr_admission;
 
 typedef struct bsr_ctx bsr_ctx;
 
@@ -237,7 +265,7 @@ int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens,
  * the store and probe are usable.  *out is NULL on failure. */
 int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out);
 
-/* Destroy a context: waits for outstanding device work of a bound request,
+/* Destroy a context: waits for outstanding device work of bound requests,
  * frees library-owned memory (arena, events, aux).  NULL is a no-op. */
 int bsr_ctx_destroy(bsr_ctx* ctx);
 
@@ -322,8 +350,15 @@ int bsr_probe(bsr_ctx* ctx, uint64_t request_id, uint64_t salt, const int32_t* t
               uint64_t n_tokens, uint32_t* n_hit_chunks, uint8_t* hit_bitmap,
               uint64_t* keys_out);
 
-/* Bind a probed request for restore and take the bounded-retrieve lock
- * (BSR_E_BUSY if another request holds it).  n_hit_chunks <= the probed n.
+/* Bind a probed request for restore.  Admission: with staging_budget_bytes
+ * B = 0 the bind takes the bounded-retrieve lock (BSR_E_BUSY while another
+ * request is bound); with B > 0 it is admitted while the rings of the bound
+ * requests plus this one (bsr_plan_staging_bytes) stay <= B and a session
+ * slot is free (else BSR_E_BUSY, retry after a commit or end; a ring larger
+ * than B alone is BSR_E_STAGING).  Concurrently bound requests need their
+ * own staging rings and status blocks (overlap -> BSR_E_ARG) and must not
+ * share destination blocks; they may share streams.  n_hit_chunks <= the
+ * probed n.
  * dst: n_groups destinations (block tables are copied to the host once and
  * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG).
  * staging: device ring of staging_bytes >= bsr_plan_staging_bytes(ctx,
@@ -365,7 +400,8 @@ int bsr_mark_group_invalid(bsr_ctx* ctx, uint64_t request_id, uint32_t group);
  * and every advertised block's valid byte = 1.  Q = 0: exposed = 0, every
  * advertised block in every group invalid, fallback = 1, and the request's
  * force-local marker is set.  Then waits for the compute stream, reads the
- * status back, releases store references and the bounded-retrieve lock.
+ * status back, releases store references and the request's admission (the
+ * lock, or its share of B).
  * Returns BSR_OK in both cases; exposed_tokens / fallback (either may be
  * NULL) report which.  All windows need not have been restored: a commit
  * before the last window exposes nothing (the prefix is incomplete). */
@@ -384,17 +420,26 @@ int bsr_invalidate(bsr_ctx* ctx, uint64_t request_id, int32_t reason);
 int bsr_request_running(bsr_ctx* ctx, uint64_t request_id);
 
 /* Request teardown: completes an uncommitted bound request (waits for its
- * device work), releases references and the lock, clears the force-local
- * marker and forgets the request's plan. */
+ * device work), releases references and its admission, clears the
+ * force-local marker and forgets the request's plan and counters. */
 int bsr_request_end(bsr_ctx* ctx, uint64_t request_id);
 
-/* Counters of the most recent bound request. */
+/* Counters of the request most recently bound or completed on this context
+ * (live while it is bound). */
 int bsr_stats_get(bsr_ctx* ctx, bsr_stats* out);
+
+/* Counters of request_id: live while it is bound, then those of its last
+ * completion until bsr_request_end or its next probe.  BSR_E_NOTFOUND if
+ * the request has neither. */
+int bsr_request_stats(bsr_ctx* ctx, uint64_t request_id, bsr_stats* out);
+
+/* Admission state: B, session slots, what is bound now and the peaks. */
+int bsr_admission_get(bsr_ctx* ctx, bsr_admission* out);
 
 /* ---- instrumentation ----------------------------------------------------------- */
 
-/* Arm one host-side fault for the next restore: `kind` BSR_INJECT_* at chunk
- * `chunk` with parameter `param`; BSR_INJECT_NONE disarms. */
+/* Arm one host-side fault for the next request bound: `kind` BSR_INJECT_*
+ * at chunk `chunk` with parameter `param`; BSR_INJECT_NONE disarms. */
 int bsr_debug_inject(bsr_ctx* ctx, int32_t kind, uint32_t chunk, uint32_t param);
 
 /* Pinned host -> device bandwidth of this context's device: best of `reps`

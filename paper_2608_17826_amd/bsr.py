@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libbsr.so")
 
 BSR_MAX_GROUPS = 8
 BSR_MAX_INSTALL_BATCH = 32
+BSR_MAX_BOUND_REQUESTS = 16
 BSR_NO_CHUNK = 0xFFFFFFFF
 
 BSR_OK = 0
@@ -35,7 +36,7 @@ BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR = 0, 1, 2
 BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
 BSR_FILE_DIRECT = 1
 
-_STRUCT_IDS = {"layout": 1, "config": 2, "group_dst": 3, "dev_status": 4, "stats": 5}
+_STRUCT_IDS = {"layout": 1, "config": 2, "group_dst": 3, "dev_status": 4, "stats": 5, "admission": 6}
 
 
 class bsr_group_desc(ct.Structure):
@@ -51,7 +52,8 @@ class bsr_layout(ct.Structure):
 class bsr_config(ct.Structure):
     _fields_ = [("window_chunks", ct.c_uint32), ("install_batch", ct.c_uint32),
                 ("hip_device", ct.c_int32), ("flags", ct.c_uint32),
-                ("window_timeout_ms", ct.c_uint32), ("reserved", ct.c_uint32 * 3)]
+                ("window_timeout_ms", ct.c_uint32), ("max_bound_requests", ct.c_uint32),
+                ("staging_budget_bytes", ct.c_uint64)]
 
 
 class bsr_group_dst(ct.Structure):
@@ -79,6 +81,13 @@ class bsr_stats(ct.Structure):
                 ("install_ms_total", ct.c_double), ("install_ms_max", ct.c_double),
                 ("host_bounce_bytes", ct.c_uint64), ("file_tier_chunks", ct.c_uint32),
                 ("reserved0", ct.c_uint32)]
+
+
+class bsr_admission(ct.Structure):
+    _fields_ = [("staging_budget_bytes", ct.c_uint64), ("max_bound_requests", ct.c_uint32),
+                ("n_bound", ct.c_uint32), ("bound_staging_bytes", ct.c_uint64),
+                ("peak_bound_staging_bytes", ct.c_uint64), ("peak_n_bound", ct.c_uint32),
+                ("n_refused", ct.c_uint32), ("aux_device_bytes", ct.c_uint64)]
 
 
 class BsrError(RuntimeError):
@@ -117,6 +126,8 @@ def _load() -> ct.CDLL:
         "bsr_request_running": (ct.c_int, [VP, U64]),
         "bsr_request_end": (ct.c_int, [VP, U64]),
         "bsr_stats_get": (ct.c_int, [VP, P(bsr_stats)]),
+        "bsr_request_stats": (ct.c_int, [VP, U64, P(bsr_stats)]),
+        "bsr_admission_get": (ct.c_int, [VP, P(bsr_admission)]),
         "bsr_debug_inject": (ct.c_int, [VP, I32, U32, U32]),
         "bsr_measure_h2d": (ct.c_int, [VP, U64, U32, U32, P(ct.c_double)]),
         "bsr_file_tier_open": (ct.c_int, [VP, ct.c_char_p, U32, U32, U32]),
@@ -130,7 +141,7 @@ def _load() -> ct.CDLL:
         f = getattr(lib, name)
         f.restype, f.argtypes = res, args
     for name, cls in (("layout", bsr_layout), ("config", bsr_config), ("group_dst", bsr_group_dst),
-                      ("dev_status", bsr_dev_status), ("stats", bsr_stats)):
+                      ("dev_status", bsr_dev_status), ("stats", bsr_stats), ("admission", bsr_admission)):
         n = lib.bsr_struct_size(_STRUCT_IDS[name])
         if n != ct.sizeof(cls):
             raise ImportError(f"struct {name}: library size {n} != binding size {ct.sizeof(cls)}")
@@ -199,10 +210,11 @@ def bsr_chunk_keys(salt: int, tokens: np.ndarray, chunk_tokens: int) -> np.ndarr
 
 # ---- context ------------------------------------------------------------------
 class Ctx:
-    """A bsr_ctx* with the layout and window it was created with."""
+    """A bsr_ctx* with the layout, window and admission budget it was created with."""
 
-    def __init__(self, handle: int, layout: bsr_layout, window_chunks: int):
+    def __init__(self, handle: int, layout: bsr_layout, window_chunks: int, staging_budget_bytes: int = 0):
         self.handle, self.layout, self.window_chunks = handle, layout, window_chunks
+        self.staging_budget_bytes = staging_budget_bytes
 
     @property
     def _as_parameter_(self):  # lets ctypes pass a Ctx where bsr_ctx* is expected
@@ -210,11 +222,13 @@ class Ctx:
 
 
 def bsr_ctx_create(layout: bsr_layout, window_chunks: int, hip_device: int = 0,
-                   install_batch: int = 0, flags: int = 0, window_timeout_ms: int = 0) -> Ctx:
-    cfg = bsr_config(window_chunks, install_batch, hip_device, flags, window_timeout_ms)
+                   install_batch: int = 0, flags: int = 0, window_timeout_ms: int = 0,
+                   staging_budget_bytes: int = 0, max_bound_requests: int = 0) -> Ctx:
+    cfg = bsr_config(window_chunks, install_batch, hip_device, flags, window_timeout_ms,
+                     max_bound_requests, staging_budget_bytes)
     out = ct.c_void_p()
     _check(_lib.bsr_ctx_create(ct.byref(layout), ct.byref(cfg), ct.byref(out)))
-    return Ctx(out.value, layout, window_chunks)
+    return Ctx(out.value, layout, window_chunks, staging_budget_bytes)
 
 
 def bsr_ctx_destroy(ctx: Ctx) -> None:
@@ -311,6 +325,18 @@ def bsr_stats_get(ctx: int) -> dict:
     s = bsr_stats()
     _check(_lib.bsr_stats_get(ctx, ct.byref(s)))
     return {name: getattr(s, name) for name, _ in bsr_stats._fields_}
+
+
+def bsr_request_stats(ctx: Ctx, request_id: int) -> dict:
+    s = bsr_stats()
+    _check(_lib.bsr_request_stats(ctx, request_id, ct.byref(s)))
+    return {name: getattr(s, name) for name, _ in bsr_stats._fields_}
+
+
+def bsr_admission_get(ctx: Ctx) -> dict:
+    a = bsr_admission()
+    _check(_lib.bsr_admission_get(ctx, ct.byref(a)))
+    return {name: getattr(a, name) for name, _ in bsr_admission._fields_}
 
 
 def bsr_debug_inject(ctx: Ctx, kind: int, chunk: int = 0, param: int = 0) -> None:

@@ -6,7 +6,8 @@
 //   probe             §3 "Probe globally", §4 probe_only lookup
 //   window loop       §2 "Bounded installation" (Eqs. 3-4), §3 "Install
 //                     locally", §4 windowed retrieve
-//   bounded lock      §3 "Install locally" (one bounded restore at a time)
+//   admission         §3 "Install locally" (one bounded restore at a time),
+//                     or §7's global budget B over the bound requests' rings
 //   commit/invalidate §3 Eq. 6 and Prop. 2, §4 "vLLM failure integration"
 //   force-local       §3 "Recover without re-entering the same fault"
 //
@@ -303,11 +304,32 @@ struct Request {
   std::vector<uint8_t> tier;  // per chunk: the tier the probe found it in
   uint32_t n_probe = 0;
   Phase phase = Phase::Probed;
+  uint64_t probe_ns = 0;
+  bool has_stats = false;  // counters of its last completion
+  bsr_stats stats{};
 };
 
-struct Session {  // the bound request
+struct Inject {
+  int32_t kind = BSR_INJECT_NONE;
+  uint32_t chunk = 0;
+  uint32_t param = 0;
+};
+
+// Device and host resources of one session slot, allocated when the context
+// is created so that binding a request allocates nothing (whole-plan mode
+// grows its event vectors at bind).
+struct SessionRes {
+  TagPair* partials = nullptr;            // per-wave tag partials of one install launch
+  bsr::VerifyAux* verify_aux = nullptr;   // verify words
+  bsr_dev_status* host_status = nullptr;  // pinned mirror of the status block
+  std::vector<hipEvent_t> full_ev, free_ev;
+  bool in_use = false;
+};
+
+struct Session {  // one bound request
   uint64_t id = 0;
-  bool active = false;
+  uint32_t res = 0;            // session slot
+  uint64_t ring_bytes = 0;     // its share of the admission budget
   uint32_t n_hit = 0;
   uint32_t window = 0;  // slots of this request's ring: W, or n_hit in whole-plan mode
   uint32_t next_chunk = 0;
@@ -328,12 +350,8 @@ struct Session {  // the bound request
   // chunks copied but not yet installed (the current install batch)
   std::vector<uint32_t> pend;
   std::vector<std::array<uint64_t, BSR_MAX_GROUPS>> pend_tags;
-};
-
-struct Inject {
-  int32_t kind = BSR_INJECT_NONE;
-  uint32_t chunk = 0;
-  uint32_t param = 0;
+  Inject inject;   // armed before this request was bound
+  bsr_stats st{};  // this request's counters
 };
 
 }  // namespace
@@ -350,15 +368,17 @@ struct bsr_ctx {
   std::unordered_set<uint64_t> force_local;
   bool tier0_available = true;
   bsr::FileTier ftier;
-  Session s;
-  bsr_stats stats{};
-  Inject inject;
-  // device resources
-  TagPair* partials = nullptr;      // per-wave tag partials of one install launch
-  uint64_t partials_bytes = 0;
-  bsr::VerifyAux* verify_aux = nullptr;
-  bsr_dev_status* host_status = nullptr;  // pinned mirror
-  std::vector<hipEvent_t> full_ev, free_ev, start_ev;
+  // admission: the lock (budget 0) or the global budget B
+  uint64_t budget = 0;
+  std::vector<SessionRes> res;                  // session slots
+  std::unordered_map<uint64_t, Session> bound;  // request id -> its session
+  uint64_t bound_bytes = 0, peak_bound_bytes = 0;
+  uint32_t peak_bound = 0, n_refused = 0;
+  uint64_t last_id = 0;   // request most recently bound or completed
+  bsr_stats last{};       // its counters when it is no longer bound
+  Inject inject;          // armed for the next bind
+  uint64_t partials_bytes = 0;  // per session slot
+  uint64_t aux_bytes = 0;       // device bytes per session slot
   std::vector<hipEvent_t> timing_pool;
 };
 
@@ -385,22 +405,29 @@ hipEvent_t take_timing_event(bsr_ctx* c) {
   return e;
 }
 
-void release_refs(bsr_ctx* c) {
-  for (uint32_t b : c->s.refs) {
+void release_refs(bsr_ctx* c, Session& s) {
+  for (uint32_t b : s.refs) {
     if (c->store.meta[b].refs) --c->store.meta[b].refs;
     c->store.maybe_free(b);
   }
-  c->s.refs.clear();
+  s.refs.clear();
+}
+
+Session* find_bound(bsr_ctx* c, uint64_t request_id) {
+  auto it = c->bound.find(request_id);
+  return it == c->bound.end() ? nullptr : &it->second;
 }
 
 // Enqueue install + verify for the chunks staged since the last flush.
-int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags) {
+int flush_batch(bsr_ctx* c, Session& s) {
+  std::vector<uint32_t>& chunks = s.pend;
+  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags = s.pend_tags;
   if (chunks.empty()) return BSR_OK;
-  Session& s = c->s;
-  const uint32_t E = static_cast<uint32_t>(c->full_ev.size());
+  SessionRes& r = c->res[s.res];
+  const uint32_t E = static_cast<uint32_t>(r.full_ev.size());
   const int64_t seq = s.batch_seq++;
-  hipEvent_t full = c->full_ev[seq % E];
-  hipEvent_t freed = c->free_ev[seq % E];
+  hipEvent_t full = r.full_ev[seq % E];
+  hipEvent_t freed = r.free_ev[seq % E];
   int rc;
   if ((rc = hip_check(hipEventRecord(full, s.copy), "hipEventRecord(full)"))) return rc;
   if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
@@ -418,9 +445,9 @@ int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::arra
     return rc;
   if (t0 && t1) s.timing.emplace_back(t0, t1);
   VerifyParams vp{};
-  vp.partials = c->partials;
+  vp.partials = r.partials;
   vp.status = s.status;
-  vp.aux = c->verify_aux;
+  vp.aux = r.verify_aux;
   vp.n_chunks = ip.n_chunks;
   vp.first_chunk = ip.first_chunk;
   vp.n_groups = c->geo.L.n_groups;
@@ -431,30 +458,29 @@ int flush_batch(bsr_ctx* c, std::vector<uint32_t>& chunks, std::vector<std::arra
   if ((rc = hip_check(bsr::launch_verify(vp, s.compute), "verify launch"))) return rc;
   if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
   for (uint32_t ch : chunks) s.slot_free_seq[ch % s.window] = seq;
-  c->stats.n_install_launches++;
-  c->stats.installed_bytes += static_cast<uint64_t>(chunks.size()) * c->geo.chunk_payload;
+  s.st.n_install_launches++;
+  s.st.installed_bytes += static_cast<uint64_t>(chunks.size()) * c->geo.chunk_payload;
   chunks.clear();
   tags.clear();
   return BSR_OK;
 }
 
-int enqueue_finish(bsr_ctx* c, uint32_t mode, uint32_t reason, uint32_t chunk, uint32_t mask) {
+int enqueue_finish(bsr_ctx* c, Session& s, uint32_t mode, uint32_t reason, uint32_t chunk, uint32_t mask) {
   // chunks still waiting for their install go first (stream order)
-  if (int rc = flush_batch(c, c->s.pend, c->s.pend_tags)) return rc;
-  FinishParams fp = c->s.fp;
+  if (int rc = flush_batch(c, s)) return rc;
+  FinishParams fp = s.fp;
   fp.mode = mode;
   fp.reason = reason;
   fp.chunk = chunk;
   fp.group_mask = mask;
-  return hip_check(bsr::launch_finish(fp, c->s.compute), "finish launch");
+  return hip_check(bsr::launch_finish(fp, s.compute), "finish launch");
 }
 
 // Host-detected failure: invalidate the whole advertised prefix.
-int host_fail(bsr_ctx* c, int reason, uint32_t chunk, uint32_t mask, int code) {
-  Session& s = c->s;
+int host_fail(bsr_ctx* c, Session& s, int reason, uint32_t chunk, uint32_t mask, int code) {
   const std::string msg = g_err;
   c->ftier.drain();  // no read of this request may still target a bounce buffer
-  int rc = enqueue_finish(c, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), chunk, mask);
+  int rc = enqueue_finish(c, s, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), chunk, mask);
   s.failed = true;
   if (s.host_fail == BSR_FAIL_NONE) s.host_fail = reason;
   c->force_local.insert(s.id);
@@ -479,6 +505,7 @@ uint64_t bsr_struct_size(int32_t which) {
     case BSR_STRUCT_GROUP_DST: return sizeof(bsr_group_dst);
     case BSR_STRUCT_DEV_STATUS: return sizeof(bsr_dev_status);
     case BSR_STRUCT_STATS: return sizeof(bsr_stats);
+    case BSR_STRUCT_ADMISSION: return sizeof(bsr_admission);
     default: return 0;
   }
 }
@@ -520,13 +547,26 @@ int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens, uint
   return BSR_OK;
 }
 
+static void free_session_res(SessionRes& r) {
+  for (auto e : r.full_ev)
+    if (e) (void)hipEventDestroy(e);
+  for (auto e : r.free_ev)
+    if (e) (void)hipEventDestroy(e);
+  r.full_ev.clear();
+  r.free_ev.clear();
+  if (r.partials) (void)hipFree(r.partials);
+  if (r.verify_aux) (void)hipFree(r.verify_aux);
+  if (r.host_status) (void)hipHostFree(r.host_status);
+  r.partials = nullptr;
+  r.verify_aux = nullptr;
+  r.host_status = nullptr;
+}
+
 int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out) {
   if (!out) return fail_with(BSR_E_ARG, "out is NULL");
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
-  if (config->reserved[0] || config->reserved[1] || config->reserved[2])
-    return fail_with(BSR_E_ARG, "config.reserved must be 0");
   // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
   // each request's ring holds its whole plan and no slot is reused.
   const uint32_t W = config->window_chunks;
@@ -538,6 +578,23 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
                : std::max(1u, std::min(W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
   if ((W && b > W) || b > BSR_MAX_INSTALL_BATCH)
     return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
+  // admission (§3 "Install locally": one bounded restore at a time; §7: a
+  // global budget B over the rings of the bound requests)
+  const uint64_t B = config->staging_budget_bytes;
+  uint32_t M = config->max_bound_requests;
+  if (M > BSR_MAX_BOUND_REQUESTS)
+    return fail_with(BSR_E_ARG, "max_bound_requests %u exceeds %d", M, BSR_MAX_BOUND_REQUESTS);
+  const uint64_t slot_bytes = bsr_slot_bytes(layout);
+  const uint64_t min_ring = static_cast<uint64_t>(std::max(W, 1u)) * slot_bytes;
+  if (B == 0) {
+    if (M > 1) return fail_with(BSR_E_ARG, "max_bound_requests %u needs a staging budget (bounded-retrieve lock: 1)", M);
+    M = 1;
+  } else {
+    if (B < min_ring)
+      return fail_with(BSR_E_ARG, "staging budget %llu B holds no ring of %llu B", (unsigned long long)B,
+                       (unsigned long long)min_ring);
+    if (M == 0) M = static_cast<uint32_t>(std::min<uint64_t>(BSR_MAX_BOUND_REQUESTS, B / min_ring));
+  }
 
   auto* c = new (std::nothrow) bsr_ctx();
   if (!c) return fail_with(BSR_E_NOMEM, "context allocation failed");
@@ -546,11 +603,14 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   c->W = W;
   c->batch = b;
   c->device = config->hip_device;
+  c->budget = B;
   c->store.index.resize(layout->n_groups);
-  c->stats.window_chunks = W;
-  c->stats.install_batch = b;
-  c->stats.slot_bytes = c->geo.slot_bytes;
-  c->stats.staging_required_bytes = c->geo.slot_bytes * W;
+  c->last.window_chunks = W;
+  c->last.install_batch = b;
+  c->last.slot_bytes = c->geo.slot_bytes;
+  c->last.staging_required_bytes = c->geo.slot_bytes * W;
+  c->last.first_failed_chunk = BSR_NO_CHUNK;
+  c->res.resize(M);
   if (c->device >= 0) {
     int rc = BSR_OK;
     int n_dev = 0;
@@ -563,23 +623,27 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
       return rc;
     }
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
+    c->aux_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
     // event ring: the copy of chunk i waits for the release of chunk i - W,
     // recorded at most W batches earlier (W + 2 leaves a margin); whole-plan
     // contexts size it per request at bind
     const uint32_t E = W ? W + 2 : 2;
-    c->full_ev.assign(E, nullptr);
-    c->free_ev.assign(E, nullptr);
-    bool ok = hipMalloc(reinterpret_cast<void**>(&c->partials), c->partials_bytes) == hipSuccess &&
-              hipMalloc(reinterpret_cast<void**>(&c->verify_aux), sizeof(bsr::VerifyAux)) == hipSuccess &&
-              hipHostMalloc(reinterpret_cast<void**>(&c->host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
-    for (uint32_t i = 0; ok && i < E; ++i)
-      ok = hipEventCreateWithFlags(&c->full_ev[i], hipEventDisableTiming) == hipSuccess &&
-           hipEventCreateWithFlags(&c->free_ev[i], hipEventDisableTiming) == hipSuccess;
+    bool ok = true;
+    for (SessionRes& r : c->res) {
+      r.full_ev.assign(E, nullptr);
+      r.free_ev.assign(E, nullptr);
+      ok = ok && hipMalloc(reinterpret_cast<void**>(&r.partials), c->partials_bytes) == hipSuccess &&
+           hipMalloc(reinterpret_cast<void**>(&r.verify_aux), sizeof(bsr::VerifyAux)) == hipSuccess &&
+           hipHostMalloc(reinterpret_cast<void**>(&r.host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
+      for (uint32_t i = 0; ok && i < E; ++i)
+        ok = hipEventCreateWithFlags(&r.full_ev[i], hipEventDisableTiming) == hipSuccess &&
+             hipEventCreateWithFlags(&r.free_ev[i], hipEventDisableTiming) == hipSuccess;
+    }
     if (!ok) {
       bsr_ctx_destroy(c);
-      return fail_with(BSR_E_NOMEM, "device resources for W=%u could not be allocated", W);
+      return fail_with(BSR_E_NOMEM, "device resources for W=%u x %u session slots could not be allocated", W, M);
     }
-    c->stats.aux_device_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
+    c->last.aux_device_bytes = c->aux_bytes;
   }
   *out = c;
   return BSR_OK;
@@ -591,22 +655,17 @@ int bsr_ctx_destroy(bsr_ctx* c) {
   c->ftier.close();
   if (c->device >= 0) {
     (void)hipSetDevice(c->device);
-    if (c->s.active) {
-      if (c->s.copy) (void)hipStreamSynchronize(c->s.copy);
-      if (c->s.compute) (void)hipStreamSynchronize(c->s.compute);
+    for (auto& kv : c->bound) {
+      Session& s = kv.second;
+      if (s.copy) (void)hipStreamSynchronize(s.copy);
+      if (s.compute) (void)hipStreamSynchronize(s.compute);
+      for (auto& pr : s.timing) {
+        (void)hipEventDestroy(pr.first);
+        (void)hipEventDestroy(pr.second);
+      }
     }
-    for (auto e : c->full_ev)
-      if (e) (void)hipEventDestroy(e);
-    for (auto e : c->free_ev)
-      if (e) (void)hipEventDestroy(e);
-    for (auto& pr : c->s.timing) {
-      (void)hipEventDestroy(pr.first);
-      (void)hipEventDestroy(pr.second);
-    }
+    for (SessionRes& r : c->res) free_session_res(r);
     for (auto e : c->timing_pool) (void)hipEventDestroy(e);
-    if (c->partials) (void)hipFree(c->partials);
-    if (c->verify_aux) (void)hipFree(c->verify_aux);
-    if (c->host_status) (void)hipHostFree(c->host_status);
     if (c->store.owned && c->store.arena) (void)hipHostFree(c->store.arena);
   }
   delete c;
@@ -745,7 +804,7 @@ int bsr_probe(bsr_ctx* c, uint64_t request_id, uint64_t salt, const int32_t* tok
   uint32_t n_hit = 0;
   {
     std::lock_guard<std::mutex> lk(c->mu);
-    if (c->s.active && c->s.id == request_id)
+    if (c->bound.count(request_id))
       return fail_with(BSR_E_STATE, "request %llu is bound; end it before probing again", (unsigned long long)request_id);
     const bool local = c->force_local.count(request_id) != 0;
     bool prefix = true;
@@ -768,9 +827,9 @@ int bsr_probe(bsr_ctx* c, uint64_t request_id, uint64_t salt, const int32_t* tok
       if (prefix) ++n_hit;
     }
     req.n_probe = n_hit;
+    req.probe_ns = now_ns() - t0;
     if (keys_out && N) std::memcpy(keys_out, req.keys.data(), N * 8);
     c->requests[request_id] = std::move(req);
-    c->stats.probe_ns = now_ns() - t0;
   }
   *n_hit_chunks = n_hit;
   return BSR_OK;
@@ -784,8 +843,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  if (c->s.active)
-    return fail_with(BSR_E_BUSY, "request %llu holds the bounded-retrieve lock", (unsigned long long)c->s.id);
+  if (c->bound.count(request_id)) return fail_with(BSR_E_STATE, "request %llu is already bound", (unsigned long long)request_id);
   auto it = c->requests.find(request_id);
   if (it == c->requests.end()) return fail_with(BSR_E_STATE, "request %llu was not probed", (unsigned long long)request_id);
   Request& rq = it->second;
@@ -802,11 +860,46 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     return fail_with(BSR_E_STAGING, "staging %llu B < W x slot = %llu B", (unsigned long long)staging_bytes, (unsigned long long)need);
   if (reinterpret_cast<uintptr_t>(staging) % 256) return fail_with(BSR_E_ARG, "staging must be 256-byte aligned");
 
+  // admission: the bounded-retrieve lock, or the global budget B
+  if (c->budget == 0) {
+    if (!c->bound.empty()) {
+      ++c->n_refused;
+      return fail_with(BSR_E_BUSY, "request %llu holds the bounded-retrieve lock",
+                       (unsigned long long)c->bound.begin()->first);
+    }
+  } else if (need > c->budget) {
+    return fail_with(BSR_E_STAGING, "ring of %llu B exceeds the staging budget %llu B", (unsigned long long)need,
+                     (unsigned long long)c->budget);
+  } else if (c->bound_bytes + need > c->budget) {
+    ++c->n_refused;
+    return fail_with(BSR_E_BUSY, "staging budget: %llu B bound + %llu B > %llu B", (unsigned long long)c->bound_bytes,
+                     (unsigned long long)need, (unsigned long long)c->budget);
+  }
+  uint32_t slot_res = 0;
+  while (slot_res < c->res.size() && c->res[slot_res].in_use) ++slot_res;
+  if (slot_res == c->res.size()) {
+    ++c->n_refused;
+    return fail_with(BSR_E_BUSY, "all %zu session slots are bound", c->res.size());
+  }
+  // concurrently bound requests must not share a ring or a status block
+  {
+    const uintptr_t r0 = reinterpret_cast<uintptr_t>(staging), r1 = r0 + need;
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(status), s1 = s0 + sizeof(bsr_dev_status);
+    for (auto& kv : c->bound) {
+      const Session& o = kv.second;
+      const uintptr_t o0 = reinterpret_cast<uintptr_t>(o.staging), o1 = o0 + o.ring_bytes;
+      const uintptr_t p0 = reinterpret_cast<uintptr_t>(o.status), p1 = p0 + sizeof(bsr_dev_status);
+      if ((r0 < o1 && o0 < r1) || (s0 < p1 && p0 < s1) || (r0 < p1 && p0 < r1) || (s0 < o1 && o0 < s1))
+        return fail_with(BSR_E_ARG, "staging or status overlaps that of bound request %llu", (unsigned long long)kv.first);
+    }
+  }
+  SessionRes& res = c->res[slot_res];
+
   const uint32_t G = c->geo.L.n_groups, C = c->geo.L.chunk_tokens;
   hipStream_t compute = static_cast<hipStream_t>(compute_stream);
   FinishParams fp{};
   fp.status = status;
-  fp.verify_aux = c->verify_aux;
+  fp.verify_aux = res.verify_aux;
   fp.n_groups = G;
   fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
   InstallParams ip{};
@@ -820,7 +913,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   std::memcpy(ip.wg_start, c->geo.wg_start, sizeof ip.wg_start);
   std::memcpy(ip.order, c->geo.order, sizeof ip.order);
   ip.lds_bytes = c->geo.lds_bytes;
-  ip.partials = c->partials;
+  ip.partials = res.partials;
   ip.status = status;
   uint32_t total = 0;
   std::vector<int32_t> bt;
@@ -856,30 +949,18 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   }
   fp.total_blocks = total;
 
-  Session& s = c->s;
-  s = Session{};
-  s.id = request_id;
-  s.n_hit = n_hit;
-  s.staging = static_cast<uint8_t*>(staging);
-  s.status = status;
-  s.copy = static_cast<hipStream_t>(copy_stream);
-  s.compute = compute;
-  s.ip = ip;
-  s.fp = fp;
-  s.window = window;
-  s.slot_free_seq.assign(window, -1);
-  s.slot_used.assign(window, 0);
-
   if (c->W == 0) {
     // whole-plan mode: one event pair per install batch of the plan
     const uint32_t E = (n_hit + c->batch - 1) / c->batch + 2;
-    while (c->full_ev.size() < E) {
+    while (res.full_ev.size() < E) {
       hipEvent_t a = nullptr, b2 = nullptr;
-      if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess ||
-          hipEventCreateWithFlags(&b2, hipEventDisableTiming) != hipSuccess)
+      if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess) return fail_with(BSR_E_NOMEM, "event creation failed");
+      if (hipEventCreateWithFlags(&b2, hipEventDisableTiming) != hipSuccess) {
+        (void)hipEventDestroy(a);
         return fail_with(BSR_E_NOMEM, "event creation failed");
-      c->full_ev.push_back(a);
-      c->free_ev.push_back(b2);
+      }
+      res.full_ev.push_back(a);
+      res.free_ev.push_back(b2);
     }
   }
   // begin: reset the status words and clear the advertised valid bytes
@@ -887,23 +968,45 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   begin.mode = bsr::kFinishBegin;
   if (int rc = hip_check(bsr::launch_finish(begin, compute), "begin launch")) return rc;
   // no copy of this request may overwrite the ring before earlier compute work is done
-  if (int rc = hip_check(hipEventRecord(c->free_ev[0], compute), "hipEventRecord")) return rc;
-  if (int rc = hip_check(hipStreamWaitEvent(s.copy, c->free_ev[0], 0), "hipStreamWaitEvent")) return rc;
-  s.batch_seq = 1;  // event slot 0 is used by the bind fence above
-  s.active = true;
-  rq.phase = Phase::Bound;
+  hipStream_t copy = static_cast<hipStream_t>(copy_stream);
+  if (int rc = hip_check(hipEventRecord(res.free_ev[0], compute), "hipEventRecord")) return rc;
+  if (int rc = hip_check(hipStreamWaitEvent(copy, res.free_ev[0], 0), "hipStreamWaitEvent")) return rc;
 
-  bsr_stats& st = c->stats;
-  const uint64_t aux = st.aux_device_bytes;
-  st = bsr_stats{};
+  Session& s = c->bound[request_id];
+  s = Session{};
+  s.id = request_id;
+  s.res = slot_res;
+  s.ring_bytes = need;
+  s.n_hit = n_hit;
+  s.staging = static_cast<uint8_t*>(staging);
+  s.status = status;
+  s.copy = copy;
+  s.compute = compute;
+  s.ip = ip;
+  s.fp = fp;
+  s.window = window;
+  s.slot_free_seq.assign(window, -1);
+  s.slot_used.assign(window, 0);
+  s.batch_seq = 1;  // event slot 0 is used by the bind fence above
+  s.inject = c->inject;
+  c->inject = Inject{};
+  res.in_use = true;
+  rq.phase = Phase::Bound;
+  c->bound_bytes += need;
+  c->peak_bound_bytes = std::max(c->peak_bound_bytes, c->bound_bytes);
+  c->peak_bound = std::max(c->peak_bound, static_cast<uint32_t>(c->bound.size()));
+  c->last_id = request_id;
+
+  bsr_stats& st = s.st;
   st.request_id = request_id;
   st.n_hit_chunks = n_hit;
   st.window_chunks = c->W;  // 0: whole-plan mode
   st.install_batch = c->batch;
   st.slot_bytes = c->geo.slot_bytes;
   st.staging_required_bytes = need;
-  st.aux_device_bytes = aux;
+  st.aux_device_bytes = c->aux_bytes;
   st.first_failed_chunk = BSR_NO_CHUNK;
+  st.probe_ns = rq.probe_ns;
   return BSR_OK;
 }
 
@@ -914,8 +1017,10 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   if (int rc = set_device(c)) return rc;
   const uint64_t t_enter = now_ns();
   std::lock_guard<std::mutex> lk(c->mu);
-  Session& s = c->s;
-  if (!s.active || s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* sp = find_bound(c, request_id);
+  if (!sp) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session& s = *sp;
+  SessionRes& res = c->res[s.res];
   if (s.failed) return fail_with(BSR_E_STATE, "request %llu already failed", (unsigned long long)request_id);
   if (n_chunks == 0 || n_chunks > s.window) return fail_with(BSR_E_ARG, "n_chunks %u must be in 1..W=%u", n_chunks, s.window);
   if (first_chunk != s.next_chunk) return fail_with(BSR_E_STATE, "window starts at %u, expected %u", first_chunk, s.next_chunk);
@@ -925,13 +1030,12 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   const Request& rq = c->requests[request_id];
   const uint32_t G = c->geo.L.n_groups;
   const uint32_t all_mask = (G >= 32) ? 0xFFFFFFFFu : ((1u << G) - 1);
-  const uint32_t E = static_cast<uint32_t>(c->free_ev.size());
+  const uint32_t E = static_cast<uint32_t>(res.free_ev.size());
   // The install batch may span windows.  A copy into slot i mod W needs the
   // install of chunk i - W, which is never in the pending batch (it holds at
   // most install_batch - 1 <= W - 1 earlier chunks), so its release event has
   // been recorded already.
   std::vector<uint32_t>& batch = s.pend;
-  std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags = s.pend_tags;
   const uint64_t t_window = now_ns();
   int rc = BSR_OK;
 
@@ -955,17 +1059,17 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
 
   for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {
     // injected host faults (forced from the host; kernels always exit normally)
-    if (c->inject.kind == BSR_INJECT_DELAY_MS && c->inject.chunk == i)
-      std::this_thread::sleep_for(std::chrono::milliseconds(c->inject.param));
+    if (s.inject.kind == BSR_INJECT_DELAY_MS && s.inject.chunk == i)
+      std::this_thread::sleep_for(std::chrono::milliseconds(s.inject.param));
     if (deadline && now_ns() > deadline) {
-      if ((rc = flush_batch(c, batch, tags))) return rc;
+      if ((rc = flush_batch(c, s))) return rc;
       fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded at chunk %u", c->cfg.window_timeout_ms, i);
-      return host_fail(c, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
+      return host_fail(c, s, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
     }
-    if (c->inject.kind == BSR_INJECT_TRANSFER_ERROR && c->inject.chunk == i) {
-      if ((rc = flush_batch(c, batch, tags))) return rc;
+    if (s.inject.kind == BSR_INJECT_TRANSFER_ERROR && s.inject.chunk == i) {
+      if ((rc = flush_batch(c, s))) return rc;
       fail_with(BSR_E_TRANSFER, "injected transfer error at chunk %u", i);
-      return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+      return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
     }
     const uint64_t key = rq.keys[i];
     const bool from_file = rq.tier[i] == kTierFile;
@@ -988,9 +1092,9 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
         if (!c->ftier.available || !c->ftier.tag(key, g, &tg[g])) missing |= 1u << g;
     }
     if (missing) {
-      if ((rc = flush_batch(c, batch, tags))) return rc;
+      if ((rc = flush_batch(c, s))) return rc;
       fail_with(BSR_E_MISSING, "chunk %u: entries missing for group mask 0x%x", i, missing);
-      return host_fail(c, BSR_FAIL_MISSING, i, missing, BSR_E_MISSING);
+      return host_fail(c, s, BSR_FAIL_MISSING, i, missing, BSR_E_MISSING);
     }
     uint32_t bounce = 0;
     if (from_file) {
@@ -1000,18 +1104,18 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       int os_err = 0;
       const int st = c->ftier.wait(bounce, deadline, &present, &os_err);
       if (st != bsr::FileTier::kReadOk || (present & all_mask) != all_mask) {
-        if ((rc = flush_batch(c, batch, tags))) return rc;
+        if ((rc = flush_batch(c, s))) return rc;
         if (st == bsr::FileTier::kReadPending) {
           fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded reading chunk %u", c->cfg.window_timeout_ms, i);
-          return host_fail(c, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
+          return host_fail(c, s, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
         }
         if (st == bsr::FileTier::kReadIoError) {
           fail_with(BSR_E_TRANSFER, "chunk %u: file read failed: %s", i, std::strerror(os_err));
-          return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+          return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
         }
         const uint32_t miss = st == bsr::FileTier::kReadOk ? (all_mask & ~present) : all_mask;
         fail_with(BSR_E_MISSING, "chunk %u: file entry missing for group mask 0x%x", i, miss);
-        return host_fail(c, BSR_FAIL_MISSING, i, miss, BSR_E_MISSING);
+        return host_fail(c, s, BSR_FAIL_MISSING, i, miss, BSR_E_MISSING);
       }
       src_block = c->ftier.bounce_data(bounce);
     } else {
@@ -1029,7 +1133,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     const uint32_t slot = i % s.window;
     const int64_t need_seq = s.slot_free_seq[slot];
     if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
-      if ((rc = hip_check(hipStreamWaitEvent(s.copy, c->free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
+      if ((rc = hip_check(hipStreamWaitEvent(s.copy, res.free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
       s.copy_waited_seq = need_seq;
     }
     uint8_t* dst = s.staging + static_cast<uint64_t>(slot) * c->geo.slot_bytes;
@@ -1049,32 +1153,32 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
         c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
         ++f_sub;
       }
-      ++c->stats.file_tier_chunks;
+      ++s.st.file_tier_chunks;
     }
     if (e != hipSuccess) {
       const std::string why = hipGetErrorString(e);
-      if ((rc = flush_batch(c, batch, tags))) return rc;
+      if ((rc = flush_batch(c, s))) return rc;
       fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
-      return host_fail(c, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+      return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
     }
-    c->stats.h2d_bytes += c->geo.slot_bytes;
+    s.st.h2d_bytes += c->geo.slot_bytes;
     if (!s.slot_used[slot]) {
       s.slot_used[slot] = 1;
       ++s.slots_touched;
     }
     batch.push_back(i);
-    tags.push_back(tg);
-    ++c->stats.n_chunks_enqueued;
+    s.pend_tags.push_back(tg);
+    ++s.st.n_chunks_enqueued;
     if (batch.size() == c->batch)
-      if ((rc = flush_batch(c, batch, tags))) return rc;
+      if ((rc = flush_batch(c, s))) return rc;
   }
   if (first_chunk + n_chunks == s.n_hit)
-    if ((rc = flush_batch(c, batch, tags))) return rc;  // the prefix is complete
+    if ((rc = flush_batch(c, s))) return rc;  // the prefix is complete
   s.next_chunk = first_chunk + n_chunks;
-  ++c->stats.n_windows;
-  c->stats.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
-  if (!fchunks.empty()) c->stats.host_bounce_bytes = c->ftier.bounce_bytes();
-  c->stats.enqueue_ns += now_ns() - t_enter;
+  ++s.st.n_windows;
+  s.st.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
+  if (!fchunks.empty()) s.st.host_bounce_bytes = c->ftier.bounce_bytes();
+  s.st.enqueue_ns += now_ns() - t_enter;
   return BSR_OK;
 }
 
@@ -1082,58 +1186,63 @@ int bsr_mark_group_invalid(bsr_ctx* c, uint64_t request_id, uint32_t group) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* s = find_bound(c, request_id);
+  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
   if (group >= c->geo.L.n_groups) return fail_with(BSR_E_ARG, "group %u out of range", group);
-  return enqueue_finish(c, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group);
+  return enqueue_finish(c, *s, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group);
 }
 
 int bsr_invalidate(bsr_ctx* c, uint64_t request_id, int32_t reason) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* s = find_bound(c, request_id);
+  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
   if (reason <= BSR_FAIL_NONE || reason > BSR_FAIL_ABORT) return fail_with(BSR_E_ARG, "invalid reason %d", reason);
   c->force_local.insert(request_id);
-  c->s.failed = true;
-  if (c->s.host_fail == BSR_FAIL_NONE) c->s.host_fail = reason;
-  return enqueue_finish(c, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), BSR_NO_CHUNK, 0);
+  s->failed = true;
+  if (s->host_fail == BSR_FAIL_NONE) s->host_fail = reason;
+  return enqueue_finish(c, *s, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), BSR_NO_CHUNK, 0);
 }
 
-// Wait for the bound request's device work, read its status, release it.
-static int complete_session(bsr_ctx* c, bool run_commit, uint64_t* exposed, int32_t* fallback) {
-  Session& s = c->s;
+// Wait for a bound request's device work, read its status, release its
+// references and admission.  The session is gone when this returns.
+static int complete_session(bsr_ctx* c, Session& s, bool run_commit, uint64_t* exposed, int32_t* fallback) {
+  SessionRes& res = c->res[s.res];
+  bsr_stats& st = s.st;
   int rc = BSR_OK;
   if (run_commit) {
     if (!s.failed && s.next_chunk < s.n_hit) {
       // an incomplete prefix is never exposed
-      rc = enqueue_finish(c, bsr::kFinishInvalidate, BSR_FAIL_ABORT, BSR_NO_CHUNK, 0);
+      rc = enqueue_finish(c, s, bsr::kFinishInvalidate, BSR_FAIL_ABORT, BSR_NO_CHUNK, 0);
       s.failed = true;
     }
-    if (!rc) rc = enqueue_finish(c, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
+    if (!rc) rc = enqueue_finish(c, s, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
   }
-  if (!rc) rc = flush_batch(c, s.pend, s.pend_tags);
+  if (!rc) rc = flush_batch(c, s);
   c->ftier.drain();
   const uint64_t t0 = now_ns();
-  if (!rc) rc = hip_check(hipMemcpyAsync(c->host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
+  if (!rc) rc = hip_check(hipMemcpyAsync(res.host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
   int rc2 = hip_check(hipStreamSynchronize(s.compute), "hipStreamSynchronize(compute)");
   int rc3 = hip_check(hipStreamSynchronize(s.copy), "hipStreamSynchronize(copy)");
   if (!rc) rc = rc2 ? rc2 : rc3;
-  c->stats.commit_wait_ns = now_ns() - t0;
+  st.commit_wait_ns = now_ns() - t0;
   if (!rc) {
-    const bsr_dev_status& h = *c->host_status;
-    c->stats.exposed_tokens = h.exposed_tokens;
-    c->stats.fallback = static_cast<int32_t>(h.fallback);
-    c->stats.fail_reason = static_cast<int32_t>(h.fail);
-    c->stats.first_failed_chunk = h.first_failed_chunk;
+    const bsr_dev_status& h = *res.host_status;
+    st.exposed_tokens = h.exposed_tokens;
+    st.fallback = static_cast<int32_t>(h.fallback);
+    st.fail_reason = static_cast<int32_t>(h.fail);
+    st.first_failed_chunk = h.first_failed_chunk;
     uint32_t m = 0;
     for (uint32_t g = 0; g < c->geo.L.n_groups; ++g)
       if (h.q[g]) m |= 1u << g;
-    c->stats.q_mask = m;
+    st.q_mask = m;
     if (h.fallback) c->force_local.insert(s.id);
     if (exposed) *exposed = h.exposed_tokens;
     if (fallback) *fallback = static_cast<int32_t>(h.fallback);
   } else {
     c->force_local.insert(s.id);
+    st.fallback = 1;
     if (exposed) *exposed = 0;
     if (fallback) *fallback = 1;
   }
@@ -1148,13 +1257,21 @@ static int complete_session(bsr_ctx* c, bool run_commit, uint64_t* exposed, int3
     c->timing_pool.push_back(pr.second);
   }
   s.timing.clear();
-  c->stats.install_ms_total = tot;
-  c->stats.install_ms_max = mx;
-  release_refs(c);
-  auto it = c->requests.find(s.id);
-  if (it != c->requests.end()) it->second.phase = Phase::Done;
-  s.active = false;
-  c->inject = Inject{};
+  st.install_ms_total = tot;
+  st.install_ms_max = mx;
+  release_refs(c, s);
+  const uint64_t id = s.id;
+  auto it = c->requests.find(id);
+  if (it != c->requests.end()) {
+    it->second.phase = Phase::Done;
+    it->second.has_stats = true;
+    it->second.stats = st;
+  }
+  c->last = st;
+  c->last_id = id;
+  c->bound_bytes -= s.ring_bytes;
+  res.in_use = false;
+  c->bound.erase(id);  // s is gone from here on
   return rc;
 }
 
@@ -1162,8 +1279,9 @@ int bsr_commit(bsr_ctx* c, uint64_t request_id, uint64_t* exposed_tokens, int32_
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  if (!c->s.active || c->s.id != request_id) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
-  return complete_session(c, true, exposed_tokens, fallback);
+  Session* s = find_bound(c, request_id);
+  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  return complete_session(c, *s, true, exposed_tokens, fallback);
 }
 
 int bsr_request_running(bsr_ctx* c, uint64_t request_id) {
@@ -1177,9 +1295,9 @@ int bsr_request_end(bsr_ctx* c, uint64_t request_id) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   std::lock_guard<std::mutex> lk(c->mu);
   int rc = BSR_OK;
-  if (c->s.active && c->s.id == request_id) {
+  if (Session* s = find_bound(c, request_id)) {
     if ((rc = set_device(c))) return rc;
-    rc = complete_session(c, false, nullptr, nullptr);
+    rc = complete_session(c, *s, false, nullptr, nullptr);
   }
   c->force_local.erase(request_id);
   c->requests.erase(request_id);
@@ -1259,7 +1377,37 @@ int bsr_plan_tiers(bsr_ctx* c, uint64_t request_id, uint8_t* tier_of_chunk, uint
 int bsr_stats_get(bsr_ctx* c, bsr_stats* out) {
   if (!c || !out) return fail_with(BSR_E_ARG, "ctx or out is NULL");
   std::lock_guard<std::mutex> lk(c->mu);
-  *out = c->stats;
+  const Session* s = find_bound(c, c->last_id);
+  *out = s ? s->st : c->last;
+  return BSR_OK;
+}
+
+int bsr_request_stats(bsr_ctx* c, uint64_t request_id, bsr_stats* out) {
+  if (!c || !out) return fail_with(BSR_E_ARG, "ctx or out is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (const Session* s = find_bound(c, request_id)) {
+    *out = s->st;
+    return BSR_OK;
+  }
+  auto it = c->requests.find(request_id);
+  if (it == c->requests.end() || !it->second.has_stats)
+    return fail_with(BSR_E_NOTFOUND, "no counters for request %llu", (unsigned long long)request_id);
+  *out = it->second.stats;
+  return BSR_OK;
+}
+
+int bsr_admission_get(bsr_ctx* c, bsr_admission* out) {
+  if (!c || !out) return fail_with(BSR_E_ARG, "ctx or out is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  *out = bsr_admission{};
+  out->staging_budget_bytes = c->budget;
+  out->max_bound_requests = static_cast<uint32_t>(c->res.size());
+  out->n_bound = static_cast<uint32_t>(c->bound.size());
+  out->bound_staging_bytes = c->bound_bytes;
+  out->peak_bound_staging_bytes = c->peak_bound_bytes;
+  out->peak_n_bound = c->peak_bound;
+  out->n_refused = c->n_refused;
+  out->aux_device_bytes = c->device >= 0 ? c->aux_bytes * c->res.size() : 0;
   return BSR_OK;
 }
 

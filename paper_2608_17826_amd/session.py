@@ -2,8 +2,10 @@
 
 Allocates the W-slot staging ring (exactly ``bsr_staging_bytes`` bytes) and
 the device status block with torch, creates two default-priority streams
-(copy, compute), and drives one request through bind -> restore_window x K
--> commit.  All restore work runs inside libbsr.so.
+(copy, compute), and drives one request at a time through bind ->
+restore_window x K -> commit.  Requests bound together under a context's
+admission budget each use a session of their own (their own ring, status
+block and streams).  All restore work runs inside libbsr.so.
 """
 
 from __future__ import annotations
@@ -69,6 +71,11 @@ class RestoreSession:
                              self.staging_bytes, self.status.data_ptr(),
                              self.copy_stream.cuda_stream, self.compute_stream.cuda_stream)
 
+    def commit(self, request_id: int, window_errors=None) -> Outcome:
+        exposed, fallback = bsr.bsr_commit(self.ctx, request_id)
+        return Outcome(exposed, fallback, list(window_errors or []), bsr.bsr_request_stats(self.ctx, request_id),
+                       status_dict(self.status))
+
     def windows(self, n_hit: int) -> List[Tuple[int, int]]:
         W = self.ctx.window_chunks or max(1, n_hit)
         return [(s, min(W, n_hit - s)) for s in range(0, n_hit, W)]
@@ -91,5 +98,4 @@ class RestoreSession:
                 break
         if before_commit is not None:
             before_commit()
-        exposed, fallback = bsr.bsr_commit(self.ctx, request_id)
-        return Outcome(exposed, fallback, errors, bsr.bsr_stats_get(self.ctx), status_dict(self.status))
+        return self.commit(request_id, errors)

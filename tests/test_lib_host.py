@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol():
     nm = subprocess.run(["nm", "-D", "--defined-only", bsr.LIB_PATH], capture_output=True, text=True).stdout
     exported = set(re.findall(r" T (bsr_[a-z0-9_]+)", nm))
     assert set(names) <= exported
-    assert bsr.bsr_abi_version() == 1
+    assert bsr.bsr_abi_version() == 2
 
 
 def _layout(w):
@@ -195,3 +195,35 @@ def test_argument_and_state_errors():
         assert "arena" in bsr.bsr_last_error()
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_admission_config_errors_and_defaults():
+    """Global admission budget B (§7): argument checks and the automatic slot count."""
+    w = get_config(2)
+    L = _layout(w)
+    c = 9_707_520
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(L, 4, hip_device=-1, max_bound_requests=2)         # lock: one slot
+    assert e.value.code == bsr.BSR_E_ARG
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(L, 4, hip_device=-1, staging_budget_bytes=4 * c - 1)  # holds no ring
+    assert e.value.code == bsr.BSR_E_ARG
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(L, 4, hip_device=-1, staging_budget_bytes=1 << 40,
+                           max_bound_requests=bsr.BSR_MAX_BOUND_REQUESTS + 1)
+    assert e.value.code == bsr.BSR_E_ARG
+    for W, B, M, want in [(4, 0, 0, 1), (4, 0, 1, 1), (4, 4 * c, 0, 1), (4, 14 * c, 0, 3),
+                          (4, 1 << 40, 0, bsr.BSR_MAX_BOUND_REQUESTS), (4, 14 * c, 7, 7),
+                          (0, c, 0, 1), (0, 5 * c + 1, 0, 5), (0, 1 << 40, 0, bsr.BSR_MAX_BOUND_REQUESTS)]:
+        ctx = bsr.bsr_ctx_create(L, W, hip_device=-1, staging_budget_bytes=B, max_bound_requests=M)
+        try:
+            a = bsr.bsr_admission_get(ctx)
+            assert a["staging_budget_bytes"] == B and a["max_bound_requests"] == want
+            assert a["n_bound"] == a["bound_staging_bytes"] == a["peak_n_bound"] == a["n_refused"] == 0
+            assert a["aux_device_bytes"] == 0          # host-only context: no session resources
+            with pytest.raises(bsr.BsrError) as e:
+                bsr.bsr_request_stats(ctx, 7)
+            assert e.value.code == bsr.BSR_E_NOTFOUND
+            assert bsr.bsr_stats_get(ctx)["window_chunks"] == W
+        finally:
+            bsr.bsr_ctx_destroy(ctx)
