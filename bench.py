@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--direct", action="store_true", help="file tier reads with O_DIRECT")
     ap.add_argument("--concurrency-sweep", default="",
                     help="file tier only: comma-separated load concurrencies to measure as well")
+    ap.add_argument("--requests", type=int, default=1,
+                    help="requests bound at once under a global admission budget B = requests x ring "
+                         "(each with its own ring and destination pools; windows interleaved)")
     return ap.parse_args()
 
 
@@ -75,9 +78,16 @@ def main():
     kinds = {"contig": bsr.BSR_KIND_CONTIG, "planar": bsr.BSR_KIND_PLANAR}
     layout = bsr.make_layout(w.chunk_tokens, [(s.block_tokens, s.n_tensors, s.record_bytes, kinds[s.kind],
                                                s.split_bytes) for s in w.groups])
-    ctx = bsr.bsr_ctx_create(layout, W, hip_device=0, install_batch=args.install_batch,
-                             flags=bsr.BSR_FLAG_TIME_INSTALL)
+    K = args.requests
+    if K < 1 or K > bsr.BSR_MAX_BOUND_REQUESTS:
+        print(f"--requests must be in 1..{bsr.BSR_MAX_BOUND_REQUESTS}", file=sys.stderr)
+        sys.exit(2)
     slot = bsr.bsr_slot_bytes(layout)
+    held_plan = w.held_chunks if not args.held_chunks else min(args.held_chunks, w.held_chunks)
+    budget = 0 if K == 1 else K * (W or held_plan) * slot
+    ctx = bsr.bsr_ctx_create(layout, W, hip_device=0, install_batch=args.install_batch,
+                             flags=bsr.BSR_FLAG_TIME_INSTALL, staging_budget_bytes=budget,
+                             max_bound_requests=0 if K == 1 else K)
     stride = (slot + 4095) // 4096 * 4096
     held = w.held_chunks if not args.held_chunks else min(args.held_chunks, w.held_chunks)
     keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
@@ -99,11 +109,13 @@ def main():
     with ThreadPoolExecutor(8) as ex:
         list(ex.map(put, range(held)))
     log(f"[bench] tier filled in {time.time() - t0:.1f}s")
-    dev = place(wi)
+    devs = [place(wi) for _ in range(K)]   # one set of destination pools per bound request
     torch.cuda.synchronize()
-    dsts = group_dsts(dev.block_tables, dev.tensor_bases, dev.valid, wi.pool_blocks)
+    dsts_all = [group_dsts(d.block_tables, d.tensor_bases, d.valid, wi.pool_blocks) for d in devs]
+    dsts = dsts_all[0]
 
-    sess = RestoreSession(ctx)
+    sessions = [RestoreSession(ctx) for _ in range(K)]
+    sess = sessions[0]
     # the ring alone, allocated the way the session allocates it
     mem0 = torch.cuda.memory_allocated()
     probe_ring = torch.empty(bsr.bsr_plan_staging_bytes(ctx, held), dtype=torch.uint8, device="cuda")
@@ -115,6 +127,8 @@ def main():
     h2d = max(bsr.bsr_measure_h2d(ctx, 1 << 30, 1, 10), bsr.bsr_measure_h2d(ctx, 1 << 30, 2, 10))
 
     def step(rid):
+        if K > 1:
+            return step_concurrent(rid)
         n, _, _ = bsr.bsr_probe(ctx, rid, wi.salt, wi.tokens)
         t_r = time.perf_counter()
         out = sess.restore(rid, n, dsts)
@@ -122,6 +136,30 @@ def main():
         bsr.bsr_request_end(ctx, rid)
         assert out.fallback == 0 and out.exposed_tokens == n * w.chunk_tokens, out
         return n, out, t_c - t_r
+
+    def step_concurrent(rid0):
+        """K requests of the same prompt, bound together, windows interleaved round-robin."""
+        rids = [rid0 * 100 + k for k in range(K)]
+        ns = [bsr.bsr_probe(ctx, r, wi.salt, wi.tokens)[0] for r in rids]
+        t_r = time.perf_counter()
+        torch.cuda.current_stream().synchronize()
+        for r, n_k, se, d in zip(rids, ns, sessions, dsts_all):
+            se.bind(r, n_k, d)
+        plans = [se.windows(n_k) for se, n_k in zip(sessions, ns)]
+        for j in range(max(len(pl) for pl in plans)):
+            for r, pl in zip(rids, plans):
+                if j < len(pl):
+                    bsr.bsr_restore_window(ctx, r, *pl[j])
+        outs_k = [se.commit(r) for r, se in zip(rids, sessions)]
+        t_c = time.perf_counter()
+        for r, o, n_k in zip(rids, outs_k, ns):
+            bsr.bsr_request_end(ctx, r)
+            assert o.fallback == 0 and o.exposed_tokens == n_k * w.chunk_tokens, o
+        merged = outs_k[0]
+        for key in ("n_install_launches", "install_ms_total", "installed_bytes"):
+            merged.stats[key] = sum(o.stats[key] for o in outs_k)
+        merged.stats["peak_live_staging_bytes"] = sum(o.stats["peak_live_staging_bytes"] for o in outs_k)
+        return ns[0], merged, t_c - t_r
 
     for i in range(args.warmup):
         log(f"[bench] warmup step {i}")
@@ -137,7 +175,7 @@ def main():
     log(f"[bench] timed {args.steps} steps in {elapsed:.3f}s")
 
     n = outs[0][0]
-    restored = n * chunk_payload
+    restored = K * n * chunk_payload
     value = restored * args.steps / elapsed / 1e9
     restore_only = restored * args.steps / sum(o[2] for o in outs) / 1e9
     launches = sum(o[1].stats["n_install_launches"] for o in outs)
@@ -187,7 +225,7 @@ def main():
             bsr.bsr_ctx_destroy(c2)
 
     cpu = None
-    if not args.no_cpu_baseline and W > 0:
+    if not args.no_cpu_baseline and W > 0 and K == 1:
         cpu = cpu_baseline(wi, W, args.cpu_seconds)
 
     line = {
@@ -206,10 +244,12 @@ def main():
         "config": {
             "workload": f"{w.name}: {w.n_tokens} tokens, {n} chunks of {w.chunk_tokens} tokens restored, "
                         f"{len(w.groups)} groups / {sum(s.n_tensors for s in w.groups)} tensors, W={W}, "
-                        "pinned-host tier -> W-slot HBM ring -> paged pools",
+                        "pinned-host tier -> W-slot HBM ring -> paged pools"
+                        + (f"; {K} requests bound together, windows interleaved" if K > 1 else ""),
             "tokens": w.n_tokens, "chunks_restored": n, "window_chunks": W,
             "chunk_bytes": slot, "restored_bytes_per_step": restored,
             "install_batch": st["install_batch"],
+            "requests": K,
             "profiling_subset": bool(args.held_chunks),
         },
         "roofline": {
@@ -227,12 +267,20 @@ def main():
         "staging": {
             "peak_live_staging_bytes": st["peak_live_staging_bytes"],
             "ring_bytes_allocated": int(ring_delta),
-            "law_W_times_chunk_bytes": (W or n) * slot,
+            "law_W_times_chunk_bytes": K * (W or n) * slot,
             "mode": "bounded window" if W else "legacy whole-plan (W=0)",
             "aux_device_bytes": st["aux_device_bytes"],
         },
         "cpu_baseline": cpu,
     }
+    if K > 1:
+        adm = bsr.bsr_admission_get(ctx)
+        line["admission"] = {"requests_bound_together": K, "staging_budget_bytes": adm["staging_budget_bytes"],
+                             "peak_bound_staging_bytes": adm["peak_bound_staging_bytes"],
+                             "peak_n_bound": adm["peak_n_bound"], "n_refused": adm["n_refused"],
+                             "aux_device_bytes": adm["aux_device_bytes"],
+                             "note": "value is the aggregate over the bound requests; staging.peak_live_"
+                                     "staging_bytes sums their rings"}
     if args.tier == "file":
         line["file_tier"] = {"dir": file_dir, "direct": bool(args.direct),
                              "load_concurrency": args.load_concurrency,
