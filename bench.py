@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=5, choices=[2, 3, 4, 5])
+    ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--window", type=int, default=32, help="W in chunks; 0 = legacy whole-plan mode")
     ap.add_argument("--install-batch", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -125,6 +125,7 @@ def main():
 
     log("[bench] measuring pinned H2D bandwidth (1 GiB, best of 10, 1 and 2 streams)")
     h2d = max(bsr.bsr_measure_h2d(ctx, 1 << 30, 1, 10), bsr.bsr_measure_h2d(ctx, 1 << 30, 2, 10))
+    copy_gbps = measure_d2d_copy(torch)
 
     def step(rid):
         if K > 1:
@@ -259,6 +260,10 @@ def main():
             "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(avg_launch_ms * 1e3, 2),
             "launches_timed": launches,
         },
+        "hbm_copy_context": {
+            "achieved": round(copy_gbps, 1), "unit": "GB/s", "frac": round(copy_gbps / HBM_PEAK_GBPS, 4),
+            "measured_as": "torch copy_ of 1 GiB device to device (read + write bytes), best of 5",
+        },
         "host_link": {
             "achieved": round(value, 3), "peak_measured": round(h2d, 3), "unit": "GB/s",
             "frac": round(value / h2d, 4), "restore_only_gbps": round(restore_only, 3),
@@ -289,6 +294,34 @@ def main():
                              "concurrency_sweep": sweep}
     print(json.dumps(line), flush=True)
     bsr.bsr_ctx_destroy(ctx)
+
+
+def measure_d2d_copy(torch):
+    """A plain device-to-device copy as context for the install kernel's HBM rate."""
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = 0.0
+    for _ in range(6):
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        e1.synchronize()
+        best = max(best, 2 * a.numel() / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del a, b
+    return best
+
+
+def host_cpu():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return f"{model}, {os.cpu_count()} logical CPUs visible"
 
 
 def open_file_tier(bsr, ctx, directory, concurrency, direct):
@@ -365,7 +398,7 @@ def cpu_baseline(wi, W, target_s):
     restored = done * layout.chunk_payload_bytes
     probe_share = t_keys * done / max(1, len(keys))
     return {"value": round(restored / (t_restore + probe_share) / 1e9, 4), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", "host": host_cpu(),
             "sample": f"first {done} of {w.held_chunks} chunks ({windows} windows of W={W}); "
                       f"{restored} bytes in {t_restore:.1f}s + pro-rated probe {probe_share:.2f}s"}
 
