@@ -1055,6 +1055,15 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     P = c->ftier.pool_size();
     for (; f_sub < fchunks.size() && f_sub < P; ++f_sub) c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
   }
+  // Whatever path leaves this call, no read it queued may still be landing in
+  // a bounce buffer: the next window (of this request or another) reuses them.
+  struct DrainReads {
+    bsr::FileTier& t;
+    const bool any;
+    ~DrainReads() {
+      if (any) t.drain();
+    }
+  } drain_reads{c->ftier, !fchunks.empty()};
   const uint64_t deadline = c->cfg.window_timeout_ms ? t_window + static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull : 0;
 
   for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {

@@ -384,3 +384,35 @@ def test_random_event_sequences_follow_the_oracle(seed):
             ts[rid].check_success()
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_file_tier_requests_share_the_bounce_pool(tmp_path):
+    """Two requests served by the file tier, bound together: their windows
+    alternate over one pool of two pinned bounce buffers."""
+    W = 4
+    wis = [_variant(2, 2 + 100 * j, n_tokens=4096) for j in range(2)]
+    layout = layout_of(wis[0])
+    ctx = bsr.bsr_ctx_create(layout, W, hip_device=0, staging_budget_bytes=2 * W * 9_707_520)
+    try:
+        slot = bsr.bsr_slot_bytes(layout)
+        bsr.bsr_store_reserve(ctx, (slot + 4095) // 4096 * 4096)   # the pinned tier stays empty
+        bsr.bsr_file_tier_open(ctx, str(tmp_path), 2, 2, 0)
+        for wi in wis:
+            keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, wi.workload.chunk_tokens)
+            with ThreadPoolExecutor(8) as ex:
+                list(ex.map(lambda i: bsr.bsr_file_tier_put_chunk(ctx, int(keys[i]), wi.payloads(i)),
+                            range(wi.workload.held_chunks)))
+        ts = [Tenant(ctx, wi, 70 + j, W) for j, wi in enumerate(wis)]
+        for t in ts:
+            assert t.probe() == 16
+            assert set(bsr.bsr_plan_tiers(ctx, t.rid, 16).tolist()) == {bsr.BSR_TIER_FILE}
+        say("case: file tier only, 2 requests bound together, 2 bounce buffers shared")
+        log = []
+        assert all(_bind(t, log) for t in ts)
+        _interleave(ts)
+        for t in ts:
+            t.commit()
+            t.check_success()
+            assert t.out.stats["file_tier_chunks"] == 16
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
