@@ -114,7 +114,7 @@ def test_random_layout_parity(seed):
             gc.close()
 
 
-@pytest.mark.parametrize("batch", [1, 3, 16])
+@pytest.mark.parametrize("batch", [1, 3, 16, 32])
 def test_config2_full_parity(batch):
     say(f"case: workload 2 (32K), W=32, install batch {batch}, full parity")
     wi = generate(get_config(2))
@@ -196,6 +196,38 @@ def test_group_fault_collapses_all_groups_and_mark_invalid():
         out = gc.restore(6, n_g, before_commit=lambda: bsr.bsr_mark_group_invalid(gc.ctx, 6, 1))
         assert res.fail_reason == oracle.FAIL_NONE
         _compare_failure(gc, case, res, out)
+    finally:
+        gc.close()
+
+
+def _eight_group_workload():
+    """BSR_MAX_GROUPS groups mixing planar and contiguous kinds and block sizes
+    that divide the chunk, exceed it, or neither; a ragged token tail."""
+    from workloads.configs import GroupSpec
+    specs = [GroupSpec("c0", 8, 2, 64, value_kind="bytes"),
+             GroupSpec("p1", 16, 1, 36, kind="planar", split_bytes=32, value_kind="bytes"),
+             GroupSpec("c2", 64, 3, 20, value_kind="bytes"),
+             GroupSpec("p3", 24, 2, 132, kind="planar", split_bytes=128, value_kind="bytes"),
+             GroupSpec("c4", 32, 1, 1152, value_kind="bytes"),
+             GroupSpec("c5", 5, 2, 12, value_kind="bytes"),
+             GroupSpec("p6", 48, 1, 24, kind="planar", split_bytes=8, value_kind="bytes"),
+             GroupSpec("c7", 128, 2, 512, value_kind="bytes")]
+    return Workload(index=300, name="eight-groups", n_tokens=40 * 32 + 7, chunk_tokens=32,
+                    groups=tuple(specs), windows=(32,), pool_factor=2)
+
+
+def test_max_groups_and_max_install_batch():
+    wi = generate(_eight_group_workload())
+    assert len(wi.workload.groups) == bsr.BSR_MAX_GROUPS
+    say("case: eight groups, W=32, install batch 32 (both maxima)")
+    case, n, _, _, res = _oracle(wi, 32)
+    assert n == 40
+    gc = GpuCase(wi, W=32, install_batch=bsr.BSR_MAX_INSTALL_BATCH)
+    try:
+        assert gc.probe(12)[0] == n
+        out = gc.restore(12, n)
+        _compare_success(gc, case, res, out)
+        assert out.stats["install_batch"] == 32 and out.stats["n_install_launches"] == 2
     finally:
         gc.close()
 
