@@ -18,6 +18,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbsr.so")
 
+BSR_ABI_VERSION = 2
 BSR_MAX_GROUPS = 8
 BSR_MAX_INSTALL_BATCH = 32
 BSR_MAX_BOUND_REQUESTS = 16
@@ -140,6 +141,8 @@ def _load() -> ct.CDLL:
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
         f.restype, f.argtypes = res, args
+    if lib.bsr_abi_version() != BSR_ABI_VERSION:
+        raise ImportError(f"libbsr.so ABI {lib.bsr_abi_version()} != binding ABI {BSR_ABI_VERSION}; rebuild")
     for name, cls in (("layout", bsr_layout), ("config", bsr_config), ("group_dst", bsr_group_dst),
                       ("dev_status", bsr_dev_status), ("stats", bsr_stats), ("admission", bsr_admission)):
         n = lib.bsr_struct_size(_STRUCT_IDS[name])
