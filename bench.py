@@ -96,9 +96,8 @@ def main():
     if args.tier == "pinned":
         log(f"[bench] pinned store: {held} chunks x {slot} B")
         bsr.bsr_store_reserve(ctx, stride * (held + 1))
-
-        def put(i):
-            bsr.bsr_store_put_chunk(ctx, int(keys[i]), wi.payloads(i))
+        # the prompt's chunks are stored together, back to back in the arena
+        bsr.bsr_store_put_chunks(ctx, keys[:held], [wi.payloads(i) for i in range(held)])
     else:
         log(f"[bench] file tier {file_dir}: {held} chunks x {slot} B, load concurrency {args.load_concurrency}")
         bsr.bsr_store_reserve(ctx, stride)
@@ -106,8 +105,8 @@ def main():
 
         def put(i):
             bsr.bsr_file_tier_put_chunk(ctx, int(keys[i]), wi.payloads(i))
-    with ThreadPoolExecutor(8) as ex:
-        list(ex.map(put, range(held)))
+        with ThreadPoolExecutor(8) as ex:
+            list(ex.map(put, range(held)))
     log(f"[bench] tier filled in {time.time() - t0:.1f}s")
     devs = [place(wi) for _ in range(K)]   # one set of destination pools per bound request
     torch.cuda.synchronize()

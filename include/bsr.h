@@ -287,6 +287,16 @@ int bsr_store_adopt(bsr_ctx* ctx, void* host_arena, uint64_t bytes);
  * the key is replaced.  BSR_E_NOMEM when the arena is full. */
 int bsr_store_put_chunk(bsr_ctx* ctx, uint64_t key, const void* const* group_payloads);
 
+/* Store n chunks, as n calls of bsr_store_put_chunk would, into arena blocks
+ * that are consecutive when the never-used part of the arena can hold all n
+ * (else into any free blocks).  keys[i] is chunk i's key; group_payloads
+ * holds n * n_groups pointers, chunk-major (chunk i, group g at
+ * i * n_groups + g).  Copies and tags run on up to 8 host threads.  Chunks
+ * of one prefix stored together sit back to back, as their staging slots do,
+ * so a restore moves runs of them with one copy each.  All or nothing:
+ * BSR_E_NOMEM (nothing stored) when fewer than n blocks are free. */
+int bsr_store_put_chunks(bsr_ctx* ctx, uint32_t n, const uint64_t* keys, const void* const* group_payloads);
+
 /* Remove the entry (key, group), or all groups of key when group < 0.  Memory
  * in use by a bound request is freed when that request ends.
  * BSR_E_NOTFOUND if no such entry. */

@@ -115,6 +115,7 @@ def _load() -> ct.CDLL:
         "bsr_store_reserve": (ct.c_int, [VP, U64]),
         "bsr_store_adopt": (ct.c_int, [VP, VP, U64]),
         "bsr_store_put_chunk": (ct.c_int, [VP, U64, P(VP)]),
+        "bsr_store_put_chunks": (ct.c_int, [VP, U32, VP, P(VP)]),
         "bsr_store_remove": (ct.c_int, [VP, U64, I32]),
         "bsr_store_payload": (ct.c_int, [VP, U64, U32, P(VP), P(U64), P(U64)]),
         "bsr_store_count": (ct.c_int, [VP, P(U64), P(U64)]),
@@ -253,6 +254,15 @@ def bsr_store_put_chunk(ctx: Ctx, key: int, payloads: Sequence[np.ndarray]) -> N
     arrs = [np.ascontiguousarray(p, dtype=np.uint8) for p in payloads]
     ptrs = (ct.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
     _check(_lib.bsr_store_put_chunk(ctx, int(key), ptrs))
+
+
+def bsr_store_put_chunks(ctx: Ctx, keys: Sequence[int], payloads: Sequence[Sequence[np.ndarray]]) -> None:
+    """payloads[i][g]: chunk i's payload of group g."""
+    n = len(keys)
+    karr = np.ascontiguousarray(np.asarray([int(k) for k in keys], dtype=np.uint64))
+    arrs = [np.ascontiguousarray(p, dtype=np.uint8) for per in payloads for p in per]
+    ptrs = (ct.c_void_p * max(1, len(arrs)))(*[a.ctypes.data for a in arrs])
+    _check(_lib.bsr_store_put_chunks(ctx, n, _ptr(karr), ptrs))
 
 
 def bsr_store_remove(ctx: Ctx, key: int, group: int = -1) -> None:

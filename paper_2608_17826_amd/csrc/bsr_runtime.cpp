@@ -748,6 +748,77 @@ int bsr_store_put_chunk(bsr_ctx* c, uint64_t key, const void* const* payloads) {
   return BSR_OK;
 }
 
+int bsr_store_put_chunks(bsr_ctx* c, uint32_t n, const uint64_t* keys, const void* const* payloads) {
+  if (!c || (n && (!keys || !payloads))) return fail_with(BSR_E_ARG, "ctx, keys or payloads is NULL");
+  if (n == 0) return BSR_OK;
+  const uint32_t G = c->geo.L.n_groups;
+  for (uint64_t i = 0; i < static_cast<uint64_t>(n) * G; ++i)
+    if (!payloads[i]) return fail_with(BSR_E_ARG, "payload of chunk %llu group %llu is NULL",
+                                       (unsigned long long)(i / G), (unsigned long long)(i % G));
+  std::vector<uint32_t> blocks(n);
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    Store& st = c->store;
+    if (!st.arena) return fail_with(BSR_E_STATE, "no store arena (reserve or adopt first)");
+    const uint64_t free_blocks = static_cast<uint64_t>(st.n_blocks - st.next_fresh) + st.free_list.size();
+    if (free_blocks < n) return fail_with(BSR_E_NOMEM, "store arena has %llu free blocks, %u needed",
+                                          (unsigned long long)free_blocks, n);
+    const bool fresh_run = st.n_blocks - st.next_fresh >= n;
+    for (uint32_t i = 0; i < n; ++i) {
+      uint32_t b;
+      if (fresh_run) {
+        b = st.next_fresh++;
+        st.meta[b] = BlockMeta{};
+        ++st.blocks_in_use;
+      } else {
+        st.alloc(&b);  // cannot fail: enough blocks were counted above
+      }
+      st.meta[b].refs = 1;  // private while it is filled
+      blocks[i] = b;
+    }
+  }
+  std::vector<uint64_t> tags(static_cast<uint64_t>(n) * G);
+  auto fill = [&](uint32_t lo, uint32_t hi) {
+    for (uint32_t i = lo; i < hi; ++i) {
+      uint8_t* base = c->store.block_ptr(blocks[i]);
+      for (uint32_t g = 0; g < G; ++g) {
+        uint8_t* dst = base + c->geo.offset[g];
+        std::memcpy(dst, payloads[static_cast<uint64_t>(i) * G + g], c->geo.payload[g]);
+        const uint64_t pad = align_up(c->geo.payload[g], kAlign) - c->geo.payload[g];
+        if (pad) std::memset(dst + c->geo.payload[g], 0, pad);
+        tags[static_cast<uint64_t>(i) * G + g] = tag_of(dst, c->geo.payload[g]);
+      }
+    }
+  };
+  unsigned nt = std::min(8u, std::max(1u, std::thread::hardware_concurrency()));
+  if (n < 2 * nt) nt = 1;
+  if (nt == 1) {
+    fill(0, n);
+  } else {
+    std::vector<std::thread> th;
+    const uint32_t per = (n + nt - 1) / nt;
+    for (unsigned t = 0; t < nt; ++t) {
+      const uint32_t lo = t * per, hi = std::min(n, lo + per);
+      if (lo < hi) th.emplace_back(fill, lo, hi);
+    }
+    for (auto& x : th) x.join();
+  }
+  std::lock_guard<std::mutex> lk(c->mu);
+  for (uint32_t i = 0; i < n; ++i) {
+    for (uint32_t g = 0; g < G; ++g) {
+      drop_entry(c, g, keys[i]);
+      c->store.index[g][keys[i]] = Entry{blocks[i], tags[static_cast<uint64_t>(i) * G + g]};
+      ++c->store.meta[blocks[i]].live_groups;
+      ++c->store.n_entries;
+    }
+  }
+  for (uint32_t i = 0; i < n; ++i) {
+    c->store.meta[blocks[i]].refs = 0;
+    c->store.maybe_free(blocks[i]);  // a key repeated within the call leaves its earlier block unused
+  }
+  return BSR_OK;
+}
+
 int bsr_store_remove(bsr_ctx* c, uint64_t key, int32_t group) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   std::lock_guard<std::mutex> lk(c->mu);
@@ -1066,17 +1137,64 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   } drain_reads{c->ftier, !fchunks.empty()};
   const uint64_t deadline = c->cfg.window_timeout_ms ? t_window + static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull : 0;
 
+  // Consecutive chunks whose pinned sources are adjacent in the arena and
+  // whose slots are adjacent in the ring are copied by one hipMemcpyAsync:
+  // every copy pays a fixed start-up cost on the copy engine that a 16 MB
+  // chunk does not amortise.  A run waits once, for the release its first
+  // chunk needs; a chunk needing a later release starts a new run, so no
+  // copy waits longer than it would alone.  A run is always issued before
+  // the batch holding its chunks is flushed, so the batch's copy event
+  // covers it.
+  struct Run {
+    const uint8_t* src = nullptr;
+    uint8_t* dst = nullptr;
+    uint64_t bytes = 0;
+    int64_t need = -1;
+    uint32_t first = 0, count = 0;
+  } run;
+  auto issue_run = [&]() -> hipError_t {
+    if (!run.count) return hipSuccess;
+    hipError_t e = hipSuccess;
+    if (run.need >= 0 && run.need > s.copy_waited_seq) {
+      e = hipStreamWaitEvent(s.copy, res.free_ev[run.need % E], 0);
+      if (e != hipSuccess) return e;
+      s.copy_waited_seq = run.need;
+    }
+    e = hipMemcpyAsync(run.dst, run.src, run.bytes, hipMemcpyHostToDevice, s.copy);
+    if (e == hipSuccess) run = Run{};
+    return e;
+  };
+  // A run whose copy could not be enqueued leaves the batch again: its chunks
+  // were never staged.
+  auto fail_run = [&](hipError_t e) -> int {
+    const std::string why = hipGetErrorString(e);
+    const uint32_t first = run.first;
+    for (uint32_t k = 0; k < run.count; ++k) {
+      batch.pop_back();
+      s.pend_tags.pop_back();
+    }
+    run = Run{};
+    if (int r2 = flush_batch(c, s)) return r2;
+    fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", first, why.c_str());
+    return host_fail(c, s, BSR_FAIL_TRANSFER, first, all_mask, BSR_E_TRANSFER);
+  };
+  // install what is staged so far: the pending run's copy first
+  auto flush_all = [&]() -> int {
+    if (hipError_t e = issue_run()) return fail_run(e);
+    return flush_batch(c, s);
+  };
+
   for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {
     // injected host faults (forced from the host; kernels always exit normally)
     if (s.inject.kind == BSR_INJECT_DELAY_MS && s.inject.chunk == i)
       std::this_thread::sleep_for(std::chrono::milliseconds(s.inject.param));
     if (deadline && now_ns() > deadline) {
-      if ((rc = flush_batch(c, s))) return rc;
+      if ((rc = flush_all())) return rc;
       fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded at chunk %u", c->cfg.window_timeout_ms, i);
       return host_fail(c, s, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
     }
     if (s.inject.kind == BSR_INJECT_TRANSFER_ERROR && s.inject.chunk == i) {
-      if ((rc = flush_batch(c, s))) return rc;
+      if ((rc = flush_all())) return rc;
       fail_with(BSR_E_TRANSFER, "injected transfer error at chunk %u", i);
       return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
     }
@@ -1101,7 +1219,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
         if (!c->ftier.available || !c->ftier.tag(key, g, &tg[g])) missing |= 1u << g;
     }
     if (missing) {
-      if ((rc = flush_batch(c, s))) return rc;
+      if ((rc = flush_all())) return rc;
       fail_with(BSR_E_MISSING, "chunk %u: entries missing for group mask 0x%x", i, missing);
       return host_fail(c, s, BSR_FAIL_MISSING, i, missing, BSR_E_MISSING);
     }
@@ -1113,7 +1231,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       int os_err = 0;
       const int st = c->ftier.wait(bounce, deadline, &present, &os_err);
       if (st != bsr::FileTier::kReadOk || (present & all_mask) != all_mask) {
-        if ((rc = flush_batch(c, s))) return rc;
+        if ((rc = flush_all())) return rc;
         if (st == bsr::FileTier::kReadPending) {
           fail_with(BSR_E_TIMEOUT, "window deadline %u ms exceeded reading chunk %u", c->cfg.window_timeout_ms, i);
           return host_fail(c, s, BSR_FAIL_TIMEOUT, i, all_mask, BSR_E_TIMEOUT);
@@ -1141,34 +1259,51 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     // the slot must have been released by the install of its previous chunk
     const uint32_t slot = i % s.window;
     const int64_t need_seq = s.slot_free_seq[slot];
-    if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
-      if ((rc = hip_check(hipStreamWaitEvent(s.copy, res.free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
-      s.copy_waited_seq = need_seq;
-    }
     uint8_t* dst = s.staging + static_cast<uint64_t>(slot) * c->geo.slot_bytes;
     hipError_t e = hipSuccess;
-    if (src_block) {
-      e = hipMemcpyAsync(dst, src_block, c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
-    } else {
-      for (uint32_t g = 0; g < G && e == hipSuccess; ++g)
-        e = hipMemcpyAsync(dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
-                           c->geo.payload[g], hipMemcpyHostToDevice, s.copy);
-    }
-    if (e == hipSuccess && from_file) {
-      // the bounce buffer is free again once this copy has run
-      e = hipEventRecord(c->ftier.bounce_event(bounce), s.copy);
-      ++f_used;
-      if (e == hipSuccess && f_sub < fchunks.size()) {
-        c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
-        ++f_sub;
+    if (!from_file && src_block) {
+      // pinned, one block: extend the run or start a new one
+      const int64_t need = need_seq > s.copy_waited_seq ? need_seq : -1;  // -1: nothing left to wait for
+      const bool extends = run.count && run.src + run.bytes == src_block && run.dst + run.bytes == dst &&
+                           need <= run.need;
+      if (!extends) {
+        if ((e = issue_run())) return fail_run(e);
+        run.src = src_block;
+        run.dst = dst;
+        run.first = i;
+        run.need = need_seq > s.copy_waited_seq ? need_seq : -1;  // issue_run may have waited
       }
-      ++s.st.file_tier_chunks;
-    }
-    if (e != hipSuccess) {
-      const std::string why = hipGetErrorString(e);
-      if ((rc = flush_batch(c, s))) return rc;
-      fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
-      return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+      run.bytes += c->geo.slot_bytes;
+      ++run.count;
+    } else {
+      if ((e = issue_run())) return fail_run(e);
+      if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
+        if ((rc = hip_check(hipStreamWaitEvent(s.copy, res.free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
+        s.copy_waited_seq = need_seq;
+      }
+      if (src_block) {
+        e = hipMemcpyAsync(dst, src_block, c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
+      } else {
+        for (uint32_t g = 0; g < G && e == hipSuccess; ++g)
+          e = hipMemcpyAsync(dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
+                             c->geo.payload[g], hipMemcpyHostToDevice, s.copy);
+      }
+      if (e == hipSuccess && from_file) {
+        // the bounce buffer is free again once this copy has run
+        e = hipEventRecord(c->ftier.bounce_event(bounce), s.copy);
+        ++f_used;
+        if (e == hipSuccess && f_sub < fchunks.size()) {
+          c->ftier.submit(static_cast<uint32_t>(f_sub % P), rq.keys[fchunks[f_sub]]);
+          ++f_sub;
+        }
+        ++s.st.file_tier_chunks;
+      }
+      if (e != hipSuccess) {
+        const std::string why = hipGetErrorString(e);
+        if ((rc = flush_batch(c, s))) return rc;
+        fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
+        return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
+      }
     }
     s.st.h2d_bytes += c->geo.slot_bytes;
     if (!s.slot_used[slot]) {
@@ -1179,8 +1314,9 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     s.pend_tags.push_back(tg);
     ++s.st.n_chunks_enqueued;
     if (batch.size() == c->batch)
-      if ((rc = flush_batch(c, s))) return rc;
+      if ((rc = flush_all())) return rc;
   }
+  if (hipError_t e = issue_run()) return fail_run(e);  // nothing of this call stays unstaged
   if (first_chunk + n_chunks == s.n_hit)
     if ((rc = flush_batch(c, s))) return rc;  // the prefix is complete
   s.next_chunk = first_chunk + n_chunks;

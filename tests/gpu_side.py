@@ -34,7 +34,7 @@ class GpuCase:
 
     def __init__(self, wi: WorkloadInputs, W: int, install_batch: int = 0, flags: int = 0,
                  timeout_ms: int = 0, held: Optional[int] = None, device: str = "cuda:0",
-                 pinned_chunks=None):
+                 pinned_chunks=None, arena_chunks: Optional[int] = None):
         self.wi = wi
         w = wi.workload
         self.layout = layout_of(wi)
@@ -44,7 +44,7 @@ class GpuCase:
         chunks = list(range(held)) if pinned_chunks is None else list(pinned_chunks)
         slot = bsr.bsr_slot_bytes(self.layout)
         stride = (slot + 4095) // 4096 * 4096
-        bsr.bsr_store_reserve(self.ctx, stride * (len(chunks) + 2))
+        bsr.bsr_store_reserve(self.ctx, stride * ((len(chunks) if arena_chunks is None else arena_chunks) + 2))
         self.keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
         self._put(chunks)
         self.dev = place(wi, device)
@@ -52,14 +52,9 @@ class GpuCase:
         self.session = RestoreSession(self.ctx, device)
 
     def _put(self, chunks) -> None:
-        def put(i):
-            bsr.bsr_store_put_chunk(self.ctx, int(self.keys[i]), self.wi.payloads(i))
-        if len(chunks) > 64:
-            with ThreadPoolExecutor(8) as ex:
-                list(ex.map(put, chunks))
-        else:
-            for i in chunks:
-                put(i)
+        if chunks:
+            bsr.bsr_store_put_chunks(self.ctx, [int(self.keys[i]) for i in chunks],
+                                     [self.wi.payloads(i) for i in chunks])
 
     def put_files(self, directory: str, chunks, concurrency: int = 2, readahead: int = 0,
                   direct: bool = False) -> None:

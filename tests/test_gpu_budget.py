@@ -130,12 +130,10 @@ def _ctx(wis, W, budget, max_bound=0):
     slot = bsr.bsr_slot_bytes(layout)
     stride = (slot + 4095) // 4096 * 4096
     bsr.bsr_store_reserve(ctx, stride * (sum(wi.workload.held_chunks for wi in wis) + 2))
-    jobs = []
     for wi in wis:
         keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, wi.workload.chunk_tokens)
-        jobs += [(wi, int(keys[i]), i) for i in range(wi.workload.held_chunks)]
-    with ThreadPoolExecutor(8) as ex:
-        list(ex.map(lambda j: bsr.bsr_store_put_chunk(ctx, j[1], j[0].payloads(j[2])), jobs))
+        held = wi.workload.held_chunks
+        bsr.bsr_store_put_chunks(ctx, keys[:held], [wi.payloads(i) for i in range(held)])
     return ctx, slot
 
 

@@ -232,6 +232,26 @@ def test_max_groups_and_max_install_batch():
         gc.close()
 
 
+def test_copy_runs_follow_the_arena_layout():
+    """Chunks stored back to back are copied in runs; a run breaks wherever
+    the arena is not contiguous (shuffled single puts, a replaced chunk)."""
+    wi = generate(get_config(2))
+    say("case: workload 2, W=32, store half bulk, half shuffled, chunk 10 replaced")
+    case, n, _, _, res = _oracle(wi, 32)
+    gc = GpuCase(wi, W=32, pinned_chunks=[], arena_chunks=130)
+    try:
+        keys = [int(k) for k in gc.keys]
+        bsr.bsr_store_put_chunks(gc.ctx, keys[:64], [wi.payloads(i) for i in range(64)])
+        for i in np.random.default_rng(7).permutation(np.arange(64, 128)):
+            bsr.bsr_store_put_chunk(gc.ctx, keys[i], wi.payloads(int(i)))
+        bsr.bsr_store_put_chunk(gc.ctx, keys[10], wi.payloads(10))   # moves to another block
+        assert gc.probe(21)[0] == n == 128
+        out = gc.restore(21, n)
+        _compare_success(gc, case, res, out)
+    finally:
+        gc.close()
+
+
 def test_empty_prefix_and_new_salt():
     wi = generate(get_config(1))
     gc = GpuCase(wi, W=2)

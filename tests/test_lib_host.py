@@ -227,3 +227,44 @@ def test_admission_config_errors_and_defaults():
             assert bsr.bsr_stats_get(ctx)["window_chunks"] == W
         finally:
             bsr.bsr_ctx_destroy(ctx)
+
+
+def test_put_chunks_matches_put_chunk_and_keeps_a_prefix_contiguous():
+    """Bulk insertion: same entries and tags as one put per chunk; the chunks
+    of one call sit in consecutive arena blocks; all or nothing when full."""
+    w = random_workload(6)
+    wi = generate(w)
+    G = len(w.groups)
+    case = build_case(wi)
+    n = w.held_chunks
+    ctx = bsr.bsr_ctx_create(_layout(w), 2, hip_device=-1)
+    slot = bsr.bsr_slot_bytes(ctx.layout)
+    stride = (slot + 4095) // 4096 * 4096
+    arena = np.zeros(stride * (n + 3), np.uint8)
+    try:
+        bsr.bsr_store_adopt(ctx, arena.ctypes.data, arena.nbytes)
+        bsr.bsr_store_put_chunk(ctx, 12345, wi.payloads(0))          # one block used first
+        bsr.bsr_store_put_chunks(ctx, case.keys[:n], [wi.payloads(i) for i in range(n)])
+        addrs = []
+        for i in range(n):
+            for g in range(G):
+                addr, nbytes, tag = bsr.bsr_store_payload(ctx, case.keys[i], g)
+                assert tag == case.store.get(case.keys[i], g)[1]
+                got = np.ctypeslib.as_array((ctypes.c_uint8 * nbytes).from_address(addr))
+                np.testing.assert_array_equal(got, wi.payload(i, g))
+            addrs.append(bsr.bsr_store_payload(ctx, case.keys[i], 0)[0])
+        assert all(b - a == stride for a, b in zip(addrs, addrs[1:]))
+        assert bsr.bsr_store_count(ctx) == (G * (n + 1), stride * (n + 1))
+        pn, _, _ = bsr.bsr_probe(ctx, 1, wi.salt, wi.tokens)
+        assert pn == oracle.probe(case.store, wi.tokens, w.chunk_tokens, wi.salt)[0]
+        # three more chunks do not fit the two free blocks: nothing is stored
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_store_put_chunks(ctx, [7, 8, 9], [wi.payloads(0)] * 3)
+        assert e.value.code == bsr.BSR_E_NOMEM
+        assert bsr.bsr_store_count(ctx)[0] == G * (n + 1)
+        # a key repeated within one call: the later payload wins, one block kept
+        bsr.bsr_store_put_chunks(ctx, [7, 7], [wi.payloads(0), wi.payloads(1)])
+        assert bsr.bsr_store_payload(ctx, 7, 0)[2] == oracle.entry_tag(wi.payload(1, 0))
+        assert bsr.bsr_store_count(ctx) == (G * (n + 2), stride * (n + 2))
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
