@@ -327,14 +327,24 @@ def open_file_tier(bsr, ctx, directory, concurrency, direct):
     bsr.bsr_file_tier_open(ctx, directory, concurrency, 0, bsr.BSR_FILE_DIRECT if direct else 0)
 
 
+KERNEL_SOURCES = ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h",
+                  "include/bsr.h")
+
+
 def kernel_sources_sha256():
+    """SHA-256 of the install kernel's sources with comments and whitespace
+    removed: a code change invalidates recorded counters, a comment does not.
+    (These sources hold no string literal containing a comment marker.)"""
     import hashlib
+    import re
 
     h = hashlib.sha256()
-    for f in ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h",
-              "include/bsr.h"):
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

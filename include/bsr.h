@@ -23,9 +23,12 @@
  *     HIP device pointers on the context's device; all others are host
  *     pointers.  Streams are hipStream_t handles passed as void*.
  *   - Sizes are in bytes unless named *_tokens, *_chunks or *_blocks.
- *   - One context serves one GPU rank.  Every call is thread safe (calls on
- *     one context are serialised by its mutex; device work of different
- *     requests overlaps on their streams).  By default one request at a time
+ *   - One context serves one GPU rank.  Every call is thread safe: calls on
+ *     one context are serialised by its mutex, except that bind (reading the
+ *     block tables back), commit and teardown do not hold it while they wait
+ *     for the device, so other requests' calls go on meanwhile; device work
+ *     of different requests overlaps on their streams.  Destroy a context
+ *     only once every other call on it has returned.  By default one request at a time
  *     may be bound (the bounded-retrieve lock of §3 "Install locally");
  *     a global admission budget B (bsr_config.staging_budget_bytes, §7) lets
  *     several be bound while their staging rings together stay within B.

@@ -1,8 +1,9 @@
 // gfx950 kernels of the bounded-window restore.
 //
 // install : scatter staged chunks from the W-slot ring into every group's
-//           paged blocks (§3 "Install locally"; §4 windowed retrieve,
-//           "performs H2D installation" of the staged window).  One
+//           paged blocks (§3 "Install locally"; §4 windowed retrieve, whose
+//           per-window step moves the staged window into the engine's
+//           blocks).  One
 //           workgroup per piece of a (tensor, destination block) segment.
 //           Contiguous groups move 16-byte vectors ring -> pool, all loads of
 //           a piece issued before its destination is resolved; planar groups

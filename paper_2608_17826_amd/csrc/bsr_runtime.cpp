@@ -334,6 +334,7 @@ struct Session {  // one bound request
   uint32_t window = 0;  // slots of this request's ring: W, or n_hit in whole-plan mode
   uint32_t next_chunk = 0;
   bool failed = false;
+  bool completing = false;  // a commit or end is waiting for its device work
   int host_fail = BSR_FAIL_NONE;
   uint8_t* staging = nullptr;
   bsr_dev_status* status = nullptr;
@@ -416,6 +417,16 @@ void release_refs(bsr_ctx* c, Session& s) {
 Session* find_bound(bsr_ctx* c, uint64_t request_id) {
   auto it = c->bound.find(request_id);
   return it == c->bound.end() ? nullptr : &it->second;
+}
+
+// The bound request the caller may act on: BSR_E_STATE when it is not bound
+// or another call is already completing it.
+int find_active(bsr_ctx* c, uint64_t request_id, Session** out) {
+  Session* s = find_bound(c, request_id);
+  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  if (s->completing) return fail_with(BSR_E_STATE, "request %llu is being completed", (unsigned long long)request_id);
+  *out = s;
+  return BSR_OK;
 }
 
 // Enqueue install + verify for the chunks staged since the last flush.
@@ -913,13 +924,9 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
                      void* compute_stream) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
-  std::lock_guard<std::mutex> lk(c->mu);
-  if (c->bound.count(request_id)) return fail_with(BSR_E_STATE, "request %llu is already bound", (unsigned long long)request_id);
-  auto it = c->requests.find(request_id);
-  if (it == c->requests.end()) return fail_with(BSR_E_STATE, "request %llu was not probed", (unsigned long long)request_id);
-  Request& rq = it->second;
-  if (rq.phase != Phase::Probed) return fail_with(BSR_E_STATE, "request %llu already bound once; probe again", (unsigned long long)request_id);
-  if (n_hit > rq.n_probe) return fail_with(BSR_E_ARG, "n_hit_chunks %u exceeds the probed prefix %u", n_hit, rq.n_probe);
+  // Arguments and block tables first, without the context lock: the
+  // readback waits for the caller's compute stream, and other requests'
+  // calls must not wait for it.  The geometry read here never changes.
   if (static_cast<uint64_t>(n_hit) * c->geo.L.chunk_tokens >= (1ull << 32))
     return fail_with(BSR_E_ARG, "a restored prefix must be shorter than 2^32 tokens");
   if (!dst || !staging || !status) return fail_with(BSR_E_ARG, "dst, staging or status is NULL");
@@ -931,46 +938,11 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     return fail_with(BSR_E_STAGING, "staging %llu B < W x slot = %llu B", (unsigned long long)staging_bytes, (unsigned long long)need);
   if (reinterpret_cast<uintptr_t>(staging) % 256) return fail_with(BSR_E_ARG, "staging must be 256-byte aligned");
 
-  // admission: the bounded-retrieve lock, or the global budget B
-  if (c->budget == 0) {
-    if (!c->bound.empty()) {
-      ++c->n_refused;
-      return fail_with(BSR_E_BUSY, "request %llu holds the bounded-retrieve lock",
-                       (unsigned long long)c->bound.begin()->first);
-    }
-  } else if (need > c->budget) {
-    return fail_with(BSR_E_STAGING, "ring of %llu B exceeds the staging budget %llu B", (unsigned long long)need,
-                     (unsigned long long)c->budget);
-  } else if (c->bound_bytes + need > c->budget) {
-    ++c->n_refused;
-    return fail_with(BSR_E_BUSY, "staging budget: %llu B bound + %llu B > %llu B", (unsigned long long)c->bound_bytes,
-                     (unsigned long long)need, (unsigned long long)c->budget);
-  }
-  uint32_t slot_res = 0;
-  while (slot_res < c->res.size() && c->res[slot_res].in_use) ++slot_res;
-  if (slot_res == c->res.size()) {
-    ++c->n_refused;
-    return fail_with(BSR_E_BUSY, "all %zu session slots are bound", c->res.size());
-  }
-  // concurrently bound requests must not share a ring or a status block
-  {
-    const uintptr_t r0 = reinterpret_cast<uintptr_t>(staging), r1 = r0 + need;
-    const uintptr_t s0 = reinterpret_cast<uintptr_t>(status), s1 = s0 + sizeof(bsr_dev_status);
-    for (auto& kv : c->bound) {
-      const Session& o = kv.second;
-      const uintptr_t o0 = reinterpret_cast<uintptr_t>(o.staging), o1 = o0 + o.ring_bytes;
-      const uintptr_t p0 = reinterpret_cast<uintptr_t>(o.status), p1 = p0 + sizeof(bsr_dev_status);
-      if ((r0 < o1 && o0 < r1) || (s0 < p1 && p0 < s1) || (r0 < p1 && p0 < r1) || (s0 < o1 && o0 < s1))
-        return fail_with(BSR_E_ARG, "staging or status overlaps that of bound request %llu", (unsigned long long)kv.first);
-    }
-  }
-  SessionRes& res = c->res[slot_res];
-
   const uint32_t G = c->geo.L.n_groups, C = c->geo.L.chunk_tokens;
   hipStream_t compute = static_cast<hipStream_t>(compute_stream);
+  hipStream_t copy = static_cast<hipStream_t>(copy_stream);
   FinishParams fp{};
   fp.status = status;
-  fp.verify_aux = res.verify_aux;
   fp.n_groups = G;
   fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
   InstallParams ip{};
@@ -984,7 +956,6 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   std::memcpy(ip.wg_start, c->geo.wg_start, sizeof ip.wg_start);
   std::memcpy(ip.order, c->geo.order, sizeof ip.order);
   ip.lds_bytes = c->geo.lds_bytes;
-  ip.partials = res.partials;
   ip.status = status;
   uint32_t total = 0;
   std::vector<int32_t> bt;
@@ -1020,6 +991,51 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   }
   fp.total_blocks = total;
 
+  std::lock_guard<std::mutex> lk(c->mu);
+  if (c->bound.count(request_id)) return fail_with(BSR_E_STATE, "request %llu is already bound", (unsigned long long)request_id);
+  auto it = c->requests.find(request_id);
+  if (it == c->requests.end()) return fail_with(BSR_E_STATE, "request %llu was not probed", (unsigned long long)request_id);
+  Request& rq = it->second;
+  if (rq.phase != Phase::Probed) return fail_with(BSR_E_STATE, "request %llu already bound once; probe again", (unsigned long long)request_id);
+  if (n_hit > rq.n_probe) return fail_with(BSR_E_ARG, "n_hit_chunks %u exceeds the probed prefix %u", n_hit, rq.n_probe);
+
+  // admission: the bounded-retrieve lock, or the global budget B
+  if (c->budget == 0) {
+    if (!c->bound.empty()) {
+      ++c->n_refused;
+      return fail_with(BSR_E_BUSY, "request %llu holds the bounded-retrieve lock",
+                       (unsigned long long)c->bound.begin()->first);
+    }
+  } else if (need > c->budget) {
+    return fail_with(BSR_E_STAGING, "ring of %llu B exceeds the staging budget %llu B", (unsigned long long)need,
+                     (unsigned long long)c->budget);
+  } else if (c->bound_bytes + need > c->budget) {
+    ++c->n_refused;
+    return fail_with(BSR_E_BUSY, "staging budget: %llu B bound + %llu B > %llu B", (unsigned long long)c->bound_bytes,
+                     (unsigned long long)need, (unsigned long long)c->budget);
+  }
+  uint32_t slot_res = 0;
+  while (slot_res < c->res.size() && c->res[slot_res].in_use) ++slot_res;
+  if (slot_res == c->res.size()) {
+    ++c->n_refused;
+    return fail_with(BSR_E_BUSY, "all %zu session slots are bound", c->res.size());
+  }
+  // concurrently bound requests must not share a ring or a status block
+  {
+    const uintptr_t r0 = reinterpret_cast<uintptr_t>(staging), r1 = r0 + need;
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(status), s1 = s0 + sizeof(bsr_dev_status);
+    for (auto& kv : c->bound) {
+      const Session& o = kv.second;
+      const uintptr_t o0 = reinterpret_cast<uintptr_t>(o.staging), o1 = o0 + o.ring_bytes;
+      const uintptr_t p0 = reinterpret_cast<uintptr_t>(o.status), p1 = p0 + sizeof(bsr_dev_status);
+      if ((r0 < o1 && o0 < r1) || (s0 < p1 && p0 < s1) || (r0 < p1 && p0 < r1) || (s0 < o1 && o0 < s1))
+        return fail_with(BSR_E_ARG, "staging or status overlaps that of bound request %llu", (unsigned long long)kv.first);
+    }
+  }
+  SessionRes& res = c->res[slot_res];
+  fp.verify_aux = res.verify_aux;
+  ip.partials = res.partials;
+
   if (c->W == 0) {
     // whole-plan mode: one event pair per install batch of the plan
     const uint32_t E = (n_hit + c->batch - 1) / c->batch + 2;
@@ -1039,7 +1055,6 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   begin.mode = bsr::kFinishBegin;
   if (int rc = hip_check(bsr::launch_finish(begin, compute), "begin launch")) return rc;
   // no copy of this request may overwrite the ring before earlier compute work is done
-  hipStream_t copy = static_cast<hipStream_t>(copy_stream);
   if (int rc = hip_check(hipEventRecord(res.free_ev[0], compute), "hipEventRecord")) return rc;
   if (int rc = hip_check(hipStreamWaitEvent(copy, res.free_ev[0], 0), "hipStreamWaitEvent")) return rc;
 
@@ -1088,8 +1103,8 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   if (int rc = set_device(c)) return rc;
   const uint64_t t_enter = now_ns();
   std::lock_guard<std::mutex> lk(c->mu);
-  Session* sp = find_bound(c, request_id);
-  if (!sp) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* sp = nullptr;
+  if (int rc0 = find_active(c, request_id, &sp)) return rc0;
   Session& s = *sp;
   SessionRes& res = c->res[s.res];
   if (s.failed) return fail_with(BSR_E_STATE, "request %llu already failed", (unsigned long long)request_id);
@@ -1331,8 +1346,8 @@ int bsr_mark_group_invalid(bsr_ctx* c, uint64_t request_id, uint32_t group) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  Session* s = find_bound(c, request_id);
-  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* s = nullptr;
+  if (int rc = find_active(c, request_id, &s)) return rc;
   if (group >= c->geo.L.n_groups) return fail_with(BSR_E_ARG, "group %u out of range", group);
   return enqueue_finish(c, *s, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group);
 }
@@ -1341,8 +1356,8 @@ int bsr_invalidate(bsr_ctx* c, uint64_t request_id, int32_t reason) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
   std::lock_guard<std::mutex> lk(c->mu);
-  Session* s = find_bound(c, request_id);
-  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
+  Session* s = nullptr;
+  if (int rc = find_active(c, request_id, &s)) return rc;
   if (reason <= BSR_FAIL_NONE || reason > BSR_FAIL_ABORT) return fail_with(BSR_E_ARG, "invalid reason %d", reason);
   c->force_local.insert(request_id);
   s->failed = true;
@@ -1351,8 +1366,12 @@ int bsr_invalidate(bsr_ctx* c, uint64_t request_id, int32_t reason) {
 }
 
 // Wait for a bound request's device work, read its status, release its
-// references and admission.  The session is gone when this returns.
-static int complete_session(bsr_ctx* c, Session& s, bool run_commit, uint64_t* exposed, int32_t* fallback) {
+// references and admission.  The context lock is dropped while the device
+// work drains, so other requests keep going; the session is marked
+// completing meanwhile, and no other call acts on it.  The session is gone
+// when this returns.
+static int complete_session(bsr_ctx* c, Session& s, std::unique_lock<std::mutex>& lk, bool run_commit,
+                            uint64_t* exposed, int32_t* fallback) {
   SessionRes& res = c->res[s.res];
   bsr_stats& st = s.st;
   int rc = BSR_OK;
@@ -1365,11 +1384,14 @@ static int complete_session(bsr_ctx* c, Session& s, bool run_commit, uint64_t* e
     if (!rc) rc = enqueue_finish(c, s, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
   }
   if (!rc) rc = flush_batch(c, s);
-  c->ftier.drain();
-  const uint64_t t0 = now_ns();
   if (!rc) rc = hip_check(hipMemcpyAsync(res.host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
-  int rc2 = hip_check(hipStreamSynchronize(s.compute), "hipStreamSynchronize(compute)");
-  int rc3 = hip_check(hipStreamSynchronize(s.copy), "hipStreamSynchronize(copy)");
+  s.completing = true;
+  const hipStream_t compute = s.compute, copy = s.copy;
+  const uint64_t t0 = now_ns();
+  lk.unlock();
+  int rc2 = hip_check(hipStreamSynchronize(compute), "hipStreamSynchronize(compute)");
+  int rc3 = hip_check(hipStreamSynchronize(copy), "hipStreamSynchronize(copy)");
+  lk.lock();
   if (!rc) rc = rc2 ? rc2 : rc3;
   st.commit_wait_ns = now_ns() - t0;
   if (!rc) {
@@ -1423,10 +1445,10 @@ static int complete_session(bsr_ctx* c, Session& s, bool run_commit, uint64_t* e
 int bsr_commit(bsr_ctx* c, uint64_t request_id, uint64_t* exposed_tokens, int32_t* fallback) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;
-  std::lock_guard<std::mutex> lk(c->mu);
-  Session* s = find_bound(c, request_id);
-  if (!s) return fail_with(BSR_E_STATE, "request %llu is not bound", (unsigned long long)request_id);
-  return complete_session(c, *s, true, exposed_tokens, fallback);
+  std::unique_lock<std::mutex> lk(c->mu);
+  Session* s = nullptr;
+  if (int rc = find_active(c, request_id, &s)) return rc;
+  return complete_session(c, *s, lk, true, exposed_tokens, fallback);
 }
 
 int bsr_request_running(bsr_ctx* c, uint64_t request_id) {
@@ -1438,11 +1460,12 @@ int bsr_request_running(bsr_ctx* c, uint64_t request_id) {
 
 int bsr_request_end(bsr_ctx* c, uint64_t request_id) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
-  std::lock_guard<std::mutex> lk(c->mu);
+  std::unique_lock<std::mutex> lk(c->mu);
   int rc = BSR_OK;
   if (Session* s = find_bound(c, request_id)) {
+    if (s->completing) return fail_with(BSR_E_STATE, "request %llu is being completed", (unsigned long long)request_id);
     if ((rc = set_device(c))) return rc;
-    rc = complete_session(c, *s, false, nullptr, nullptr);
+    rc = complete_session(c, *s, lk, false, nullptr, nullptr);
   }
   c->force_local.erase(request_id);
   c->requests.erase(request_id);
