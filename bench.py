@@ -167,9 +167,12 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] timing {args.steps} steps")
     outs = []
+    step_s = []
     t_start = time.perf_counter()
     for i in range(args.steps):
+        t_i = time.perf_counter()
         outs.append(step(2000 + i))
+        step_s.append(time.perf_counter() - t_i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     log(f"[bench] timed {args.steps} steps in {elapsed:.3f}s")
@@ -236,6 +239,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "ms_per_step_median": round(sorted(step_s)[len(step_s) // 2] * 1e3, 3),
+        "value_at_median_step": round(restored / sorted(step_s)[len(step_s) // 2] / 1e9, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
