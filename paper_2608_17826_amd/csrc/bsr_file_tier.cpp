@@ -11,6 +11,8 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
+#include <thread>
 
 namespace bsr {
 
@@ -39,11 +41,13 @@ uint64_t steady_ns() {
       .count();
 }
 
+// Reads exactly n bytes; a file that ends early fails with errno = ENODATA.
 bool full_pread(int fd, void* buf, uint64_t n, uint64_t off) {
   uint8_t* p = static_cast<uint8_t*>(buf);
   while (n) {
     const ssize_t r = pread(fd, p, n, static_cast<off_t>(off));
     if (r < 0 && errno == EINTR) continue;
+    if (r == 0) errno = ENODATA;
     if (r <= 0) return false;
     p += r;
     off += static_cast<uint64_t>(r);
@@ -131,13 +135,19 @@ int FileTier::start(int device, std::string* err) {
   slots_.assign(readahead_, Slot{});
   for (uint32_t b = 0; b < readahead_; ++b) {
     void* p = nullptr;
-    if (hipHostMalloc(&p, file_bytes_, hipHostMallocDefault) != hipSuccess ||
-        hipEventCreateWithFlags(&bounce_ev_[b], hipEventDisableTiming) != hipSuccess) {
+    const bool ok = hipHostMalloc(&p, file_bytes_, hipHostMallocDefault) == hipSuccess &&
+                    hipEventCreateWithFlags(&bounce_ev_[b], hipEventDisableTiming) == hipSuccess;
+    bounce_[b] = static_cast<uint8_t*>(p);
+    if (!ok) {
       *err = "file tier: bounce buffers could not be allocated";
-      bounce_[b] = static_cast<uint8_t*>(p);
+      for (uint32_t k = 0; k <= b; ++k) {
+        if (bounce_ev_[k]) (void)hipEventDestroy(bounce_ev_[k]);
+        if (bounce_[k]) (void)hipHostFree(bounce_[k]);
+      }
+      bounce_.clear();
+      bounce_ev_.clear();
       return -1;
     }
-    bounce_[b] = static_cast<uint8_t*>(p);
   }
   stop_ = false;
   for (uint32_t t = 0; t < concurrency_; ++t) workers_.emplace_back(&FileTier::worker, this);
@@ -208,16 +218,23 @@ int FileTier::put(uint64_t key, const void* const* payloads, const uint64_t* tag
   uint64_t t[kMaxGroups] = {};
   for (uint32_t g = 0; g < n_groups_; ++g) t[g] = tags[g];
   const uint32_t present = (n_groups_ == 32) ? 0xFFFFFFFFu : ((1u << n_groups_) - 1);
+  // write a private file, then rename it over the chunk's file: a reader
+  // sees the old file or the new one, never a partial one
   const std::string p = path_of(key);
-  const int fd = ::open(p.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
+  char suffix[48];
+  std::snprintf(suffix, sizeof suffix, ".%llx.tmp", static_cast<unsigned long long>(
+                                                        std::hash<std::thread::id>()(std::this_thread::get_id())));
+  const std::string tmp = p + suffix;
+  const int fd = ::open(tmp.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
   if (fd < 0) {
-    *err = "cannot write " + p + ": " + std::strerror(errno);
+    *err = "cannot write " + tmp + ": " + std::strerror(errno);
     return -1;
   }
   const bool ok = write_header(fd, key, present, t) == 0 && full_pwrite(fd, body.data(), body.size(), kHeaderBytes);
   ::close(fd);
-  if (!ok) {
-    *err = "short write to " + p;
+  if (!ok || ::rename(tmp.c_str(), p.c_str()) != 0) {
+    *err = (ok ? "cannot rename " : "short write to ") + tmp;
+    ::unlink(tmp.c_str());
     return -1;
   }
   std::lock_guard<std::mutex> lk(imu_);
@@ -322,7 +339,7 @@ void FileTier::worker() {
     } else {
       if (!full_pread(fd, land, file_bytes_, 0)) {
         err = errno;
-        status = kReadIoError;
+        status = err == ENODATA ? kReadMissing : kReadIoError;  // a truncated file holds no complete object
       } else {
         if (land != bounce_[t.b]) std::memcpy(bounce_[t.b], land, file_bytes_);
         Header h{};

@@ -160,3 +160,32 @@ def test_file_entry_removed_after_probe(tmp_path, k):
         np.testing.assert_array_equal(gc.valid_host(0), case.valid[0])
     finally:
         _free(gc)
+
+
+@pytest.mark.parametrize("k", [3, 15])
+def test_file_truncated_after_probe(tmp_path, k):
+    """A chunk file cut short after the probe holds no complete object: its
+    window fails as missing (§4: a retrieve requires complete presence)."""
+    say(f"case: workload 1 from files, chunk {k}'s file truncated after the probe")
+    wi = generate(get_config(1))
+    allc = range(16)
+
+    def drop(ts, keys):
+        for g in range(len(wi.workload.groups)):
+            ts[1].store.remove(keys[k], g)
+
+    case, n, ct, res = _oracle_tiers(wi, [], allc, W=2, after_probe=drop)
+    gc = GpuCase(wi, W=2, pinned_chunks=[])
+    try:
+        gc.put_files(str(tmp_path), allc, concurrency=2, readahead=4)
+        n_g, _, keys = gc.probe(21)
+        path = tmp_path / f"{int(keys[k]):016x}.bsr"
+        with open(path, "r+b") as f:
+            f.truncate(4096 + 1000)                  # the header survives, the body does not
+        out = gc.restore(21, n_g)
+        assert out.exposed_tokens == 0 and out.fallback == 1
+        assert out.status["fail"] == bsr.BSR_FAIL_MISSING
+        assert out.status["first_failed_chunk"] == res.first_failed_chunk == k
+        np.testing.assert_array_equal(gc.valid_host(0), case.valid[0])
+    finally:
+        _free(gc)

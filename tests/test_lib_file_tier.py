@@ -93,3 +93,36 @@ def test_probe_tier_choice_matches_oracle(tmp_path):
         assert list(bsr.bsr_plan_tiers(ctx, 100, 16)) == [0] * 10 + [1] * 6
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_file_replace_is_atomic(tmp_path):
+    """Concurrent replacements of one chunk file leave exactly one complete
+    version (each writer renames a private file over it) and no leftovers."""
+    from concurrent.futures import ThreadPoolExecutor
+    w = random_workload(5)
+    wi = generate(w)
+    G = len(w.groups)
+    ctx, arena = _ctx(w, tmp_path, 1)
+    try:
+        versions = [wi.payloads(i) for i in range(min(4, w.held_chunks))]
+        with ThreadPoolExecutor(4) as ex:
+            list(ex.map(lambda v: bsr.bsr_file_tier_put_chunk(ctx, 77, v), versions * 3))
+        assert os.listdir(tmp_path) == [f"{77:016x}.bsr"]
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
+    # the file on disk is one whole version: its header tags match one payload set
+    raw = (tmp_path / f"{77:016x}.bsr").read_bytes()
+    tags = np.frombuffer(raw[40:40 + 8 * G], dtype="<u8")
+    want = [[oracle.entry_tag(p) for p in v] for v in versions]
+    assert [int(t) for t in tags] in want
+    i = want.index([int(t) for t in tags])
+    ctx2, arena2 = _ctx(w, tmp_path, 1)
+    try:
+        assert bsr.bsr_file_tier_count(ctx2) == G
+    finally:
+        bsr.bsr_ctx_destroy(ctx2)
+    slot_off = 4096
+    layout = oracle.OracleLayout.from_specs(w.chunk_tokens, w.groups)
+    for g in range(G):
+        off = slot_off + layout.group_offsets()[g]
+        np.testing.assert_array_equal(np.frombuffer(raw[off:off + layout.payload_bytes(g)], np.uint8), versions[i][g])
