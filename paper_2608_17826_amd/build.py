@@ -33,6 +33,22 @@ def _run(cmd):
     return r
 
 
+C_CONSUMER_SRC = os.path.join(ROOT, "tests", "c_abi", "gpu_restore.cpp")
+C_CONSUMER = os.path.join(ROOT, "tests", "c_abi", "gpu_restore")
+
+
+def build_c_consumer(verbose: bool = False) -> str:
+    """The torch-free test consumer of the C ABI, linked against libbsr.so
+    (found next to the package via a relative rpath)."""
+    tmp = C_CONSUMER + ".tmp"
+    _run([HIPCC, "-O2", "-std=c++17", f"-I{INCLUDE}", C_CONSUMER_SRC, f"-L{PKG}", "-lbsr",
+          "-Wl,-rpath,$ORIGIN/../../paper_2608_17826_amd", "-o", tmp])
+    os.replace(tmp, C_CONSUMER)
+    if verbose:
+        print("built", C_CONSUMER)
+    return C_CONSUMER
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = []
@@ -46,6 +62,7 @@ def build(verbose: bool = False) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)
+    build_c_consumer(verbose)
     return LIB
 
 
