@@ -268,6 +268,10 @@ def main():
             "achieved": round(copy_gbps, 1), "unit": "GB/s", "frac": round(copy_gbps / HBM_PEAK_GBPS, 4),
             "measured_as": "torch copy_ of 1 GiB device to device (read + write bytes), best of 5",
         },
+        "probe": {
+            "ms_median": round(sorted(o[1].stats["probe_ns"] for o in outs)[len(outs) // 2] / 1e6, 3),
+            "chunks": n, "note": "chunk keys + tier lookups on the host, inside each timed step",
+        },
         "host_link": {
             "achieved": round(value, 3), "peak_measured": round(h2d, 3), "unit": "GB/s",
             "frac": round(value / h2d, 4), "restore_only_gbps": round(restore_only, 3),
