@@ -89,6 +89,7 @@ extern "C" {
 #define BSR_FAIL_TIMEOUT 3
 #define BSR_FAIL_TRANSFER 4
 #define BSR_FAIL_ABORT 5
+#define BSR_FAIL_BLOCK_TABLE 6 /* an advertised block id lies outside its pool (BSR_FLAG_TRUSTED_TABLES) */
 
 /* group kinds */
 #define BSR_KIND_CONTIG 0
@@ -96,6 +97,12 @@ extern "C" {
 
 /* bsr_config.flags */
 #define BSR_FLAG_TIME_INSTALL 1u  /* time every install launch with HIP events */
+#define BSR_FLAG_TRUSTED_TABLES 2u /* bind does not read the block tables back, so it never waits for the
+                                      compute stream (an engine's model work may be queued there); the
+                                      tables are checked on the device after the begin kernel instead: an
+                                      id outside [0, pool_blocks) fails the request (fail = BSR_FAIL_BLOCK_TABLE,
+                                      nothing exposed; the kernels never write such an id).  The caller
+                                      guarantees that no id repeats within one group's prefix (not checked) */
 
 /* fault injection (bsr_debug_inject), forced from the host */
 #define BSR_INJECT_NONE 0
@@ -141,7 +148,7 @@ typedef struct bsr_config {
                                  BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
                                  windows; a batch smaller than W keeps the copy engine busy across windows */
   int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
-  uint32_t flags;             /* BSR_FLAG_* */
+  uint32_t flags;             /* BSR_FLAG_*; unknown bits are an error */
   uint32_t window_timeout_ms; /* per-window fetch deadline, 0 = none */
   uint32_t max_bound_requests;   /* session slots: requests that may be bound at once, each with its own
                                     pre-allocated tag partials, verify words, events and status mirror.
@@ -373,7 +380,9 @@ int bsr_probe(bsr_ctx* ctx, uint64_t request_id, uint64_t salt, const int32_t* t
  * share destination blocks; they may share streams.  n_hit_chunks <= the
  * probed n.
  * dst: n_groups destinations (block tables are copied to the host once and
- * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG).
+ * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG; with
+ * BSR_FLAG_TRUSTED_TABLES they are checked on the device instead, see the
+ * flag).
  * staging: device ring of staging_bytes >= bsr_plan_staging_bytes(ctx,
  * n_hit_chunks) (else BSR_E_STAGING); the library uses exactly that many.
  * status: device bsr_dev_status.  Enqueues, on compute_stream, the begin

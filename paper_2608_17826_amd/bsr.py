@@ -29,10 +29,10 @@ BSR_E_ARG, BSR_E_STATE, BSR_E_MISSING, BSR_E_CORRUPT, BSR_E_TIMEOUT = -1, -2, -3
 BSR_E_TRANSFER, BSR_E_NOMEM, BSR_E_STAGING, BSR_E_BUSY, BSR_E_DEVICE, BSR_E_NOTFOUND = -6, -7, -8, -9, -10, -11
 
 BSR_FAIL_NONE, BSR_FAIL_MISSING, BSR_FAIL_CORRUPT = 0, 1, 2
-BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT = 3, 4, 5
+BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT, BSR_FAIL_BLOCK_TABLE = 3, 4, 5, 6
 
 BSR_KIND_CONTIG, BSR_KIND_PLANAR = 0, 1
-BSR_FLAG_TIME_INSTALL = 1
+BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES = 1, 2
 BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR = 0, 1, 2
 BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
 BSR_FILE_DIRECT = 1

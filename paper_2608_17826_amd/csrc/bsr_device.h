@@ -127,6 +127,8 @@ struct GroupValid {
   uint8_t* valid;
   uint32_t n_req_blocks;    // advertised blocks of this group
   uint32_t pool_blocks;
+  uint32_t block_tokens;
+  uint32_t pad;
 };
 
 // mode of the finishing kernel
@@ -135,6 +137,7 @@ enum FinishMode : uint32_t {
   kFinishCommit = 1,      // Eq. 6: Q -> valid bytes, exposed, fallback
   kFinishInvalidate = 2,  // record failure, clear valid bytes, exposed = 0, fallback = 1
   kFinishMarkGroup = 3,   // q[group] = 0
+  kFinishCheckTables = 4, // fail the request if an advertised block id is outside its pool
 };
 
 struct FinishParams {
@@ -146,6 +149,7 @@ struct FinishParams {
   uint32_t chunk;           // invalidate: failing chunk or BSR_NO_CHUNK
   uint32_t group_mask;      // invalidate: groups whose q_g becomes 0; mark: the group
   uint32_t total_blocks;    // sum of n_req_blocks
+  uint32_t chunk_tokens;
   uint64_t exposed_if_valid;
   GroupValid g[BSR_MAX_GROUPS];
 };

@@ -18,7 +18,7 @@
 //           groups).
 // finish  : begin (reset status, clear advertised valid bytes), commit
 //           (Eq. 6), invalidate (§4 failed-block + HMA-aware invalidation),
-//           mark one group invalid.
+//           mark one group invalid, check the block tables on the device.
 //
 // Nothing here is a dense contraction: the path is bound by HBM bandwidth
 // (read the staged chunk once, write the paged blocks once).
@@ -351,6 +351,26 @@ __global__ __launch_bounds__(256) void k_finish(const FinishParams p) {
   uint8_t value = 0;
   if (p.mode == kFinishMarkGroup) {
     if (gid == 0) st->q[p.group_mask] = 0;
+    return;
+  }
+  if (p.mode == kFinishCheckTables) {
+    // runs after begin, before any install: an advertised block id outside
+    // its pool fails the request (the installs and commit never write it)
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t idx = gid; idx < p.total_blocks; idx += stride) {
+      uint32_t g = 0, k = idx;
+      while (g + 1 < p.n_groups && k >= p.g[g].n_req_blocks) {
+        k -= p.g[g].n_req_blocks;
+        ++g;
+      }
+      const int32_t b = p.g[g].block_table[k];
+      if (b < 0 || static_cast<uint32_t>(b) >= p.g[g].pool_blocks) {
+        atomicCAS(&st->fail, static_cast<uint32_t>(BSR_FAIL_NONE), static_cast<uint32_t>(BSR_FAIL_BLOCK_TABLE));
+        atomicMin(&st->first_failed_chunk,
+                  static_cast<uint32_t>(static_cast<uint64_t>(k) * p.g[g].block_tokens / p.chunk_tokens));
+        st->q[g] = 0;
+      }
+    }
     return;
   }
   if (p.mode == kFinishBegin) {

@@ -578,6 +578,8 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
+  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES))
+    return fail_with(BSR_E_ARG, "unknown config flags 0x%x", config->flags);
   // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
   // each request's ring holds its whole plan and no slot is reused.
   const uint32_t W = config->window_chunks;
@@ -944,7 +946,9 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   FinishParams fp{};
   fp.status = status;
   fp.n_groups = G;
+  fp.chunk_tokens = C;
   fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
+  const bool trusted = (c->cfg.flags & BSR_FLAG_TRUSTED_TABLES) != 0;
   InstallParams ip{};
   ip.ring = static_cast<const uint8_t*>(staging);
   ip.slot_bytes = c->geo.slot_bytes;
@@ -966,19 +970,21 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     if (!d.block_table || !d.tensor_bases || !d.valid) return fail_with(BSR_E_ARG, "group %u: NULL destination pointer", g);
     if (d.n_blocks < nreq) return fail_with(BSR_E_ARG, "group %u: block table has %u blocks, prefix needs %llu", g, d.n_blocks, (unsigned long long)nreq);
     if (d.pool_blocks == 0) return fail_with(BSR_E_ARG, "group %u: pool_blocks is 0", g);
-    // copy the advertised part of the block table back once and check it
-    bt.resize(nreq);
-    if (nreq) {
-      int rc = hip_check(hipMemcpyAsync(bt.data(), d.block_table, nreq * 4, hipMemcpyDeviceToHost, compute), "block table readback");
-      if (!rc) rc = hip_check(hipStreamSynchronize(compute), "hipStreamSynchronize");
-      if (rc) return rc;
-    }
-    std::vector<uint8_t> seen(d.pool_blocks, 0);
-    for (uint64_t k = 0; k < nreq; ++k) {
-      const int32_t b = bt[k];
-      if (b < 0 || static_cast<uint32_t>(b) >= d.pool_blocks)
-        return fail_with(BSR_E_ARG, "group %u: block_table[%llu] = %d outside [0, %u)", g, (unsigned long long)k, b, d.pool_blocks);
-      if (seen[b]++) return fail_with(BSR_E_ARG, "group %u: block %d appears twice in the prefix", g, b);
+    if (!trusted) {
+      // copy the advertised part of the block table back once and check it
+      bt.resize(nreq);
+      if (nreq) {
+        int rc = hip_check(hipMemcpyAsync(bt.data(), d.block_table, nreq * 4, hipMemcpyDeviceToHost, compute), "block table readback");
+        if (!rc) rc = hip_check(hipStreamSynchronize(compute), "hipStreamSynchronize");
+        if (rc) return rc;
+      }
+      std::vector<uint8_t> seen(d.pool_blocks, 0);
+      for (uint64_t k = 0; k < nreq; ++k) {
+        const int32_t b = bt[k];
+        if (b < 0 || static_cast<uint32_t>(b) >= d.pool_blocks)
+          return fail_with(BSR_E_ARG, "group %u: block_table[%llu] = %d outside [0, %u)", g, (unsigned long long)k, b, d.pool_blocks);
+        if (seen[b]++) return fail_with(BSR_E_ARG, "group %u: block %d appears twice in the prefix", g, b);
+      }
     }
     GroupGeom q = c->geo.gg[g];
     q.pool_blocks = d.pool_blocks;
@@ -986,7 +992,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     q.block_table = d.block_table;
     q.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
     ip.g[g] = q;
-    fp.g[g] = bsr::GroupValid{d.block_table, d.valid, static_cast<uint32_t>(nreq), d.pool_blocks};
+    fp.g[g] = bsr::GroupValid{d.block_table, d.valid, static_cast<uint32_t>(nreq), d.pool_blocks, B, 0};
     total += static_cast<uint32_t>(nreq);
   }
   fp.total_blocks = total;
@@ -1054,6 +1060,11 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   FinishParams begin = fp;
   begin.mode = bsr::kFinishBegin;
   if (int rc = hip_check(bsr::launch_finish(begin, compute), "begin launch")) return rc;
+  if (trusted) {
+    FinishParams check = fp;
+    check.mode = bsr::kFinishCheckTables;
+    if (int rc = hip_check(bsr::launch_finish(check, compute), "block table check launch")) return rc;
+  }
   // no copy of this request may overwrite the ring before earlier compute work is done
   if (int rc = hip_check(hipEventRecord(res.free_ev[0], compute), "hipEventRecord")) return rc;
   if (int rc = hip_check(hipStreamWaitEvent(copy, res.free_ev[0], 0), "hipStreamWaitEvent")) return rc;

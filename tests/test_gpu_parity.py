@@ -252,6 +252,52 @@ def test_copy_runs_follow_the_arena_layout():
         gc.close()
 
 
+@pytest.mark.parametrize("seed", [0, 4, 9])
+def test_trusted_tables_parity(seed):
+    """BSR_FLAG_TRUSTED_TABLES: no block-table readback at bind; same image."""
+    w = random_workload(seed)
+    wi = generate(w)
+    W = w.windows[1]
+    say(f"case: trusted tables, random layout seed={seed} W={W}")
+    case, n, _, _, res = _oracle(wi, W)
+    gc = GpuCase(wi, W=W, flags=bsr.BSR_FLAG_TRUSTED_TABLES)
+    try:
+        assert gc.probe(31)[0] == n
+        out = gc.restore(31, n)
+        _compare_success(gc, case, res, out)
+    finally:
+        gc.close()
+
+
+@pytest.mark.parametrize("bad", ["past_pool", "negative"])
+def test_trusted_tables_bad_id_fails_closed(bad):
+    """An advertised id outside its pool, unchecked at bind, fails the request
+    on the device: nothing is written, nothing is exposed (Prop. 2)."""
+    wi = generate(get_config(1))
+    say(f"case: trusted tables, workload 1, block_table[37] {bad}")
+    gc = GpuCase(wi, W=2, flags=bsr.BSR_FLAG_TRUSTED_TABLES)
+    try:
+        pb = wi.pool_blocks[0]
+        gc.dev.block_tables[0][37] = pb if bad == "past_pool" else -5
+        torch.cuda.synchronize()
+        n = gc.probe(32)[0]
+        out = gc.restore(32, n)
+        assert out.exposed_tokens == 0 and out.fallback == 1
+        assert out.status["fail"] == bsr.BSR_FAIL_BLOCK_TABLE
+        assert out.status["first_failed_chunk"] == 37 * 16 // 64
+        assert out.status["q"][0] == 0
+        # no install ran: every pool byte keeps its sentinel
+        np.testing.assert_array_equal(gc.pool_host(0), wi.sentinel_pool(0))
+        # every advertised in-range block is invalid, the rest untouched
+        want = wi.valid_init[0].copy()
+        bt = wi.block_tables[0]
+        want[np.delete(bt, 37)] = 0
+        np.testing.assert_array_equal(gc.valid_host(0), want)
+        assert gc.probe(32)[0] == 0          # force-local after the fallback
+    finally:
+        gc.close()
+
+
 def test_empty_prefix_and_new_salt():
     wi = generate(get_config(1))
     gc = GpuCase(wi, W=2)

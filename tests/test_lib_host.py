@@ -268,3 +268,13 @@ def test_put_chunks_matches_put_chunk_and_keeps_a_prefix_contiguous():
         assert bsr.bsr_store_count(ctx) == (G * (n + 2), stride * (n + 2))
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_unknown_config_flags_are_rejected():
+    w = get_config(2)
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(_layout(w), 4, hip_device=-1, flags=0x80)
+    assert e.value.code == bsr.BSR_E_ARG
+    ctx = bsr.bsr_ctx_create(_layout(w), 4, hip_device=-1,
+                             flags=bsr.BSR_FLAG_TIME_INSTALL | bsr.BSR_FLAG_TRUSTED_TABLES)
+    bsr.bsr_ctx_destroy(ctx)
