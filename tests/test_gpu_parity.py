@@ -171,6 +171,62 @@ def test_config1_failure_parity(mode, k):
         gc.close()
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_random_layout_failure_parity(seed):
+    """Random layouts x a seeded fault (missing / corrupt entry in a random
+    group, timeout, transfer error, abort) at a seeded chunk."""
+    w = random_workload(seed)
+    wi = generate(w)
+    rng = np.random.default_rng(500 + seed)
+    W = int(rng.choice(w.windows))
+    G = len(w.groups)
+    n_full = w.n_full_chunks
+    k = int(rng.integers(0, n_full))
+    g = int(rng.integers(0, G))
+    n_windows = -(-n_full // W)
+    mode = ["missing", "corrupt", "timeout", "transfer", "abort"][seed % 5]
+    if mode == "abort" and n_windows < 2:
+        W = max(1, n_full // 2)                 # at least two windows to abort after the first
+        n_windows = -(-n_full // W)
+        if n_windows < 2:
+            mode = "missing"
+    layout = oracle.OracleLayout.from_specs(w.chunk_tokens, w.groups)
+    byte = int(rng.integers(0, layout.payload_bytes(g)))
+    mask = int(rng.integers(1, 256))
+    abort_k = int(rng.integers(1, n_windows)) if mode == "abort" else None
+    say(f"case: random layout seed={seed} W={W} fault {mode} chunk {k} group {g}")
+    kw = {}
+    if mode == "missing":
+        mut = lambda case, keys: case.store.remove(keys[k], g)  # noqa: E731
+    elif mode == "corrupt":
+        mut = lambda case, keys: case.store.corrupt(keys[k], g, byte, mask)  # noqa: E731
+    else:
+        mut = None
+    if mode in ("timeout", "transfer"):
+        kw["faults"] = {k: oracle.FAIL_TIMEOUT if mode == "timeout" else oracle.FAIL_TRANSFER}
+    if mode == "abort":
+        kw["abort_after_windows"] = abort_k
+    case, n, _, _, res = _oracle(wi, W, mutate=mut, **kw)
+    assert n == n_full
+    gc = GpuCase(wi, W=W, timeout_ms=50 if mode == "timeout" else 0)
+    try:
+        n_g, _, keys = gc.probe(40)
+        assert n_g == n
+        if mode == "missing":
+            bsr.bsr_store_remove(gc.ctx, int(keys[k]), g)
+        elif mode == "corrupt":
+            gc.corrupt(int(keys[k]), g, byte, mask)
+        elif mode == "timeout":
+            bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_DELAY_MS, k, 200)
+        elif mode == "transfer":
+            bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_TRANSFER_ERROR, k, 0)
+        out = gc.restore(40, n_g, abort_after_windows=abort_k)
+        _compare_failure(gc, case, res, out)
+        assert gc.probe(40)[0] == 0
+    finally:
+        gc.close()
+
+
 def test_group_fault_collapses_all_groups_and_mark_invalid():
     say("case: workload-2 layout, 6 chunks, group B missing at 3; then group marked invalid")
     w0 = get_config(2)
