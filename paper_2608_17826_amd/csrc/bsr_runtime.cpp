@@ -15,6 +15,9 @@
 // slot, copy stream) waits for the event that released the slot's previous
 // chunk; its install (compute stream) waits for the batch's copies.  The
 // device therefore never holds more than W staged chunks, whatever N is.
+// Copies of chunks adjacent in the arena and in the ring go out together.
+// Each bound request has its own session slot (tag partials, verify words,
+// events, status mirror), allocated with the context.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -252,7 +255,7 @@ struct Entry {
 
 struct BlockMeta {
   uint32_t live_groups = 0;  // index entries pointing here
-  uint32_t refs = 0;         // references held by the bound request
+  uint32_t refs = 0;         // references held by bound requests
 };
 
 struct Store {
