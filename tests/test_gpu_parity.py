@@ -354,14 +354,19 @@ def test_trusted_tables_bad_id_fails_closed(bad):
         gc.close()
 
 
-def test_empty_prefix_and_new_salt():
+@pytest.mark.parametrize("W", [2, 0])
+def test_empty_prefix_and_new_salt(W):
+    """n = 0: nothing staged, nothing exposed, no fallback; in whole-plan mode
+    (W = 0) the ring of an empty plan is one slot."""
     wi = generate(get_config(1))
-    gc = GpuCase(wi, W=2)
+    gc = GpuCase(wi, W=W)
     try:
         n, bm, _ = gc.probe(8, salt=wi.salt + 2)
         assert n == 0 and not bm.any()
         out = gc.restore(8, 0)
         assert out.exposed_tokens == 0 and out.fallback == 0
+        assert out.stats["staging_required_bytes"] == max(W, 1) * 147_456
+        assert out.stats["peak_live_staging_bytes"] == 0 and out.stats["h2d_bytes"] == 0
         for g in range(1):
             np.testing.assert_array_equal(gc.valid_host(g), wi.valid_init[g])
             np.testing.assert_array_equal(gc.pool_host(g), wi.sentinel_pool(g))
