@@ -108,6 +108,8 @@ extern "C" {
 #define BSR_INJECT_NONE 0
 #define BSR_INJECT_DELAY_MS 1       /* sleep param ms before fetching chunk */
 #define BSR_INJECT_TRANSFER_ERROR 2 /* treat chunk's copy submission as failed */
+#define BSR_INJECT_LAUNCH_ERROR 3   /* the first install flush holding chunk reports a failed launch
+                                       (nothing is launched; one shot) */
 
 /* external tiers, in the probe's order of preference (§4 "System topology":
  * remote DRAM first, local SSD as the lower reusable tier) */

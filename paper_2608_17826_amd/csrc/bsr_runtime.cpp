@@ -437,6 +437,12 @@ int flush_batch(bsr_ctx* c, Session& s) {
   std::vector<uint32_t>& chunks = s.pend;
   std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags = s.pend_tags;
   if (chunks.empty()) return BSR_OK;
+  if (s.inject.kind == BSR_INJECT_LAUNCH_ERROR &&
+      std::find(chunks.begin(), chunks.end(), s.inject.chunk) != chunks.end()) {
+    const uint32_t at = s.inject.chunk;
+    s.inject = Inject{};  // one shot: the retry at commit launches normally
+    return fail_with(BSR_E_TRANSFER, "injected install launch failure (batch with chunk %u)", at);
+  }
   SessionRes& r = c->res[s.res];
   const uint32_t E = static_cast<uint32_t>(r.full_ev.size());
   const int64_t seq = s.batch_seq++;
@@ -488,6 +494,16 @@ int enqueue_finish(bsr_ctx* c, Session& s, uint32_t mode, uint32_t reason, uint3
   fp.chunk = chunk;
   fp.group_mask = mask;
   return hip_check(bsr::launch_finish(fp, s.compute), "finish launch");
+}
+
+// A launch or enqueue failed: the device may not hold what the host
+// enqueued, so the request can no longer be exposed.  Commit invalidates it
+// (and no further window of it is accepted).
+int launch_failed(bsr_ctx* c, Session& s, int code) {
+  s.failed = true;
+  if (s.host_fail == BSR_FAIL_NONE) s.host_fail = BSR_FAIL_TRANSFER;
+  c->force_local.insert(s.id);
+  return code;
 }
 
 // Host-detected failure: invalidate the whole advertised prefix.
@@ -1203,14 +1219,15 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       s.pend_tags.pop_back();
     }
     run = Run{};
-    if (int r2 = flush_batch(c, s)) return r2;
+    if (int r2 = flush_batch(c, s)) return launch_failed(c, s, r2);
     fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", first, why.c_str());
     return host_fail(c, s, BSR_FAIL_TRANSFER, first, all_mask, BSR_E_TRANSFER);
   };
   // install what is staged so far: the pending run's copy first
   auto flush_all = [&]() -> int {
     if (hipError_t e = issue_run()) return fail_run(e);
-    return flush_batch(c, s);
+    if (int r2 = flush_batch(c, s)) return launch_failed(c, s, r2);
+    return BSR_OK;
   };
 
   for (uint32_t i = first_chunk; i < first_chunk + n_chunks; ++i) {
@@ -1307,7 +1324,8 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     } else {
       if ((e = issue_run())) return fail_run(e);
       if (need_seq >= 0 && need_seq > s.copy_waited_seq) {
-        if ((rc = hip_check(hipStreamWaitEvent(s.copy, res.free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)"))) return rc;
+        if ((rc = hip_check(hipStreamWaitEvent(s.copy, res.free_ev[need_seq % E], 0), "hipStreamWaitEvent(free)")))
+          return launch_failed(c, s, rc);
         s.copy_waited_seq = need_seq;
       }
       if (src_block) {
@@ -1329,7 +1347,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       }
       if (e != hipSuccess) {
         const std::string why = hipGetErrorString(e);
-        if ((rc = flush_batch(c, s))) return rc;
+        if ((rc = flush_batch(c, s))) return launch_failed(c, s, rc);
         fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
         return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
       }
@@ -1347,7 +1365,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   }
   if (hipError_t e = issue_run()) return fail_run(e);  // nothing of this call stays unstaged
   if (first_chunk + n_chunks == s.n_hit)
-    if ((rc = flush_batch(c, s))) return rc;  // the prefix is complete
+    if ((rc = flush_batch(c, s))) return launch_failed(c, s, rc);  // the prefix is complete
   s.next_chunk = first_chunk + n_chunks;
   ++s.st.n_windows;
   s.st.peak_live_staging_bytes = static_cast<uint64_t>(s.slots_touched) * c->geo.slot_bytes;
@@ -1363,7 +1381,8 @@ int bsr_mark_group_invalid(bsr_ctx* c, uint64_t request_id, uint32_t group) {
   Session* s = nullptr;
   if (int rc = find_active(c, request_id, &s)) return rc;
   if (group >= c->geo.L.n_groups) return fail_with(BSR_E_ARG, "group %u out of range", group);
-  return enqueue_finish(c, *s, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group);
+  if (int rc = enqueue_finish(c, *s, bsr::kFinishMarkGroup, 0, BSR_NO_CHUNK, group)) return launch_failed(c, *s, rc);
+  return BSR_OK;
 }
 
 int bsr_invalidate(bsr_ctx* c, uint64_t request_id, int32_t reason) {
@@ -1390,9 +1409,12 @@ static int complete_session(bsr_ctx* c, Session& s, std::unique_lock<std::mutex>
   bsr_stats& st = s.st;
   int rc = BSR_OK;
   if (run_commit) {
-    if (!s.failed && s.next_chunk < s.n_hit) {
-      // an incomplete prefix is never exposed
-      rc = enqueue_finish(c, s, bsr::kFinishInvalidate, BSR_FAIL_ABORT, BSR_NO_CHUNK, 0);
+    if (s.failed || s.next_chunk < s.n_hit) {
+      // a failure the host knows of, or an incomplete prefix, is never
+      // exposed: invalidate right before the commit (on the device the first
+      // recorded failure is kept, so repeating an earlier invalidate is harmless)
+      const int reason = s.host_fail != BSR_FAIL_NONE ? s.host_fail : BSR_FAIL_ABORT;
+      rc = enqueue_finish(c, s, bsr::kFinishInvalidate, static_cast<uint32_t>(reason), BSR_NO_CHUNK, 0);
       s.failed = true;
     }
     if (!rc) rc = enqueue_finish(c, s, bsr::kFinishCommit, 0, BSR_NO_CHUNK, 0);
@@ -1595,7 +1617,7 @@ int bsr_admission_get(bsr_ctx* c, bsr_admission* out) {
 
 int bsr_debug_inject(bsr_ctx* c, int32_t kind, uint32_t chunk, uint32_t param) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
-  if (kind < BSR_INJECT_NONE || kind > BSR_INJECT_TRANSFER_ERROR) return fail_with(BSR_E_ARG, "unknown inject kind %d", kind);
+  if (kind < BSR_INJECT_NONE || kind > BSR_INJECT_LAUNCH_ERROR) return fail_with(BSR_E_ARG, "unknown inject kind %d", kind);
   std::lock_guard<std::mutex> lk(c->mu);
   c->inject = Inject{kind, chunk, param};
   return BSR_OK;

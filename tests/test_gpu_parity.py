@@ -227,6 +227,43 @@ def test_random_layout_failure_parity(seed):
         gc.close()
 
 
+def test_failed_install_launch_fails_closed_and_refuses_retries():
+    """A launch failure inside a window (forced from the host: the flush of the
+    batch holding chunk 40 reports a failed launch and launches nothing) marks
+    the request failed: a retried window is refused, and commit invalidates
+    before it commits, so nothing is exposed (Prop. 2)."""
+    wi = generate(get_config(2))
+    layout = oracle.OracleLayout.from_specs(wi.workload.chunk_tokens, wi.workload.groups)
+    say("case: workload 2, W=32, install launch failure injected at the batch holding chunk 40")
+    gc = GpuCase(wi, W=32)
+    try:
+        n = gc.probe(50)[0]
+        assert n == 128
+        bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_LAUNCH_ERROR, 40, 0)
+        torch.cuda.synchronize()
+        gc.session.bind(50, n, gc.dsts())
+        bsr.bsr_restore_window(gc.ctx, 50, 0, 32)
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_restore_window(gc.ctx, 50, 32, 32)
+        assert e.value.code == bsr.BSR_E_TRANSFER
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_restore_window(gc.ctx, 50, 32, 32)      # the same window again
+        assert e.value.code == bsr.BSR_E_STATE
+        out = gc.session.commit(50)
+        assert out.exposed_tokens == 0 and out.fallback == 1
+        assert out.status["fail"] == bsr.BSR_FAIL_TRANSFER
+        for g in range(2):
+            want = [v.copy() for v in wi.valid_init]
+            oracle.set_request_valid(layout, n, wi.block_tables, want, 0)
+            np.testing.assert_array_equal(gc.valid_host(g), want[g])
+            req = wi.block_tables[g]
+            others = np.setdiff1d(np.arange(wi.pool_blocks[g]), req)
+            np.testing.assert_array_equal(gc.pool_host(g)[:, others], wi.sentinel_pool(g)[:, others])
+        assert gc.probe(50)[0] == 0
+    finally:
+        gc.close()
+
+
 def test_group_fault_collapses_all_groups_and_mark_invalid():
     say("case: workload-2 layout, 6 chunks, group B missing at 3; then group marked invalid")
     w0 = get_config(2)
