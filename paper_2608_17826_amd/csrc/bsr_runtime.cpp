@@ -437,6 +437,8 @@ int flush_batch(bsr_ctx* c, Session& s) {
   std::vector<uint32_t>& chunks = s.pend;
   std::vector<std::array<uint64_t, BSR_MAX_GROUPS>>& tags = s.pend_tags;
   if (chunks.empty()) return BSR_OK;
+  if (chunks.size() > BSR_MAX_INSTALL_BATCH)  // the verify launch holds one expected tag row per chunk
+    return fail_with(BSR_E_STATE, "install batch of %zu chunks exceeds %d", chunks.size(), BSR_MAX_INSTALL_BATCH);
   if (s.inject.kind == BSR_INJECT_LAUNCH_ERROR &&
       std::find(chunks.begin(), chunks.end(), s.inject.chunk) != chunks.end()) {
     const uint32_t at = s.inject.chunk;
