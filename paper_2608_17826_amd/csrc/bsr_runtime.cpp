@@ -463,8 +463,11 @@ int flush_batch(bsr_ctx* c, Session& s) {
     t1 = take_timing_event(c);
     if (!t0 || !t1) t0 = t1 = nullptr;
   }
-  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute, t0, t1), "install launch")))
+  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute, t0, t1), "install launch"))) {
+    if (t0) c->timing_pool.push_back(t0);
+    if (t1) c->timing_pool.push_back(t1);
     return rc;
+  }
   if (t0 && t1) s.timing.emplace_back(t0, t1);
   VerifyParams vp{};
   vp.partials = r.partials;
