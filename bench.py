@@ -336,40 +336,49 @@ def open_file_tier(bsr, ctx, directory, concurrency, direct):
     bsr.bsr_file_tier_open(ctx, directory, concurrency, 0, bsr.BSR_FILE_DIRECT if direct else 0)
 
 
-KERNEL_SOURCES = ("paper_2608_17826_amd/csrc/bsr_kernels.hip", "paper_2608_17826_amd/csrc/bsr_device.h",
-                  "include/bsr.h")
-
-
-def kernel_sources_sha256():
-    """SHA-256 of the install kernel's sources with comments and whitespace
-    removed: a code change invalidates recorded counters, a comment does not.
-    (These sources hold no string literal containing a comment marker.)"""
+def kernel_code_sha256(lib_path=None):
+    """SHA-256 of the gfx950 code object inside libbsr.so: the kernels as
+    built.  Counters recorded against it hold exactly as long as the machine
+    code does; documentation or host-side edits leave it unchanged.  The
+    library is a clang offload bundle ("__CLANG_OFFLOAD_BUNDLE__", entry count,
+    then offset / size / triple per entry).  None if it cannot be read."""
     import hashlib
-    import re
+    import struct
 
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
-            text = fh.read()
-        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-        text = re.sub(r"//[^\n]*", " ", text)
-        h.update(" ".join(text.split()).encode())
-    return h.hexdigest()
+    path = lib_path or os.path.join(ROOT, "paper_2608_17826_amd", "libbsr.so")
+    try:
+        with open(path, "rb") as fh:
+            data = fh.read()
+    except OSError:
+        return None
+    i = data.find(b"__CLANG_OFFLOAD_BUNDLE__")
+    if i < 0:
+        return None
+    (n,) = struct.unpack_from("<Q", data, i + 24)
+    p = i + 32
+    for _ in range(n):
+        off, size, tlen = struct.unpack_from("<QQQ", data, p)
+        p += 24
+        triple = data[p:p + tlen].decode(errors="replace")
+        p += tlen
+        if triple.endswith("gfx950"):
+            return hashlib.sha256(data[i + off:i + off + size]).hexdigest()
+    return None
 
 
 def recorded_traffic(workload_name, install_batch):
     """HBM bytes per k_install launch from the committed rocprofv3 counter
-    summary, only if it was taken on the kernel sources built here."""
+    summary, only if it was taken on the kernel code built here."""
     import glob
     import re
 
-    sha = kernel_sources_sha256()
+    sha = kernel_code_sha256()
     for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
         for m in re.finditer(r"<!-- traffic-record ([^>]*) -->", open(path).read()):
             kv = dict(x.split("=", 1) for x in m.group(1).split())
             if (kv.get("kernel") == "k_install" and kv.get("workload") == workload_name
                     and int(kv.get("install_batch", -1)) == install_batch
-                    and kv.get("kernel_sources_sha256") == sha):
+                    and sha is not None and kv.get("kernel_code_sha256") == sha):
                 return int(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
     return None, None
 

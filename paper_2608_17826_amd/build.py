@@ -54,7 +54,9 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in SOURCES:
         obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        lang = ["-x", "hip"] if src.endswith(".hip") else []
+        # a fixed compilation-unit id keeps the device code object independent
+        # of where the tree is built (it is otherwise derived from the path)
+        lang = ["-x", "hip", "-cuid=" + os.path.splitext(src)[0]] if src.endswith(".hip") else []
         _run([HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     tmp = LIB + ".tmp"
