@@ -114,6 +114,29 @@ def test_random_layout_parity(seed):
             gc.close()
 
 
+@pytest.mark.parametrize("seed", range(10, 20))
+def test_random_layout_batch_and_flags_parity(seed):
+    """Random layouts with a seeded window, install batch size and block-table
+    check (host readback or device check), against the oracle image."""
+    w = random_workload(seed)
+    wi = generate(w)
+    rng = np.random.default_rng(900 + seed)
+    W = int(rng.choice(w.windows))
+    batch = int(rng.integers(1, min(W, bsr.BSR_MAX_INSTALL_BATCH) + 1))
+    flags = bsr.BSR_FLAG_TRUSTED_TABLES if rng.random() < 0.5 else 0
+    say(f"case: random layout seed={seed} W={W} install_batch={batch} flags={flags}")
+    case, n, _, _, res = _oracle(wi, W)
+    gc = GpuCase(wi, W=W, install_batch=batch, flags=flags)
+    try:
+        assert gc.probe(41)[0] == n
+        out = gc.restore(41, n)
+        _compare_success(gc, case, res, out)
+        assert out.stats["install_batch"] == batch
+        assert out.stats["n_install_launches"] == -(-n // batch) if n else True
+    finally:
+        gc.close()
+
+
 @pytest.mark.parametrize("batch", [1, 3, 16, 32])
 def test_config2_full_parity(batch):
     say(f"case: workload 2 (32K), W=32, install batch {batch}, full parity")
