@@ -148,7 +148,9 @@ typedef struct bsr_config {
                                  plan, n_hit slots, none reused; peak staging n_hit * slot bytes, Eq. 2) */
   uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W - W/8, at least 1, at most
                                  BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
-                                 windows; a batch smaller than W keeps the copy engine busy across windows */
+                                 windows; a batch smaller than W keeps the copy engine busy across windows.
+                                 BSR_E_ARG when one launch of this many chunks would exceed HIP's 2^32 - 1
+                                 work-items (a layout of very many small tensors): lower it */
   int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
   uint32_t flags;             /* BSR_FLAG_*; unknown bits are an error */
   uint32_t window_timeout_ms; /* per-window fetch deadline, 0 = none */

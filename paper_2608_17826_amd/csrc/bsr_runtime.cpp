@@ -636,6 +636,14 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   auto* c = new (std::nothrow) bsr_ctx();
   if (!c) return fail_with(BSR_E_NOMEM, "context allocation failed");
   build_geometry(layout, &c->geo);
+  // one install launch of b chunks runs b x wg_per_chunk workgroups: HIP
+  // takes at most 2^32 - 1 work-items in a grid dimension
+  if (static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallThreads >= (1ull << 32)) {
+    const uint32_t wpc = c->geo.wg_per_chunk;
+    delete c;
+    return fail_with(BSR_E_ARG, "an install launch of %u chunks x %u workgroups exceeds the grid limit; lower install_batch",
+                     b, wpc);
+  }
   c->cfg = *config;
   c->W = W;
   c->batch = b;

@@ -229,6 +229,23 @@ def test_admission_config_errors_and_defaults():
             bsr.bsr_ctx_destroy(ctx)
 
 
+def test_install_grid_limit():
+    """One install launch runs install_batch x (workgroups per chunk) workgroups
+    of 256 threads; a layout and batch whose grid would pass 2^32 - 1
+    work-items is refused at creation, and a smaller batch is accepted."""
+    def layout(n_tensors):   # one token per chunk and per block, 4-byte records: one workgroup per tensor
+        return bsr.make_layout(1, [(1, n_tensors, 4, bsr.BSR_KIND_CONTIG, 0)])
+    limit = (1 << 32) // (32 * 256)          # 524,288 tensors at the automatic batch of 32 (W = 64)
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(layout(limit), 64, hip_device=-1)
+    assert e.value.code == bsr.BSR_E_ARG and "grid limit" in bsr.bsr_last_error()
+    for n, W, b in [(limit - 1, 64, 0), (limit, 64, 16), (limit, 0, 16)]:
+        bsr.bsr_ctx_destroy(bsr.bsr_ctx_create(layout(n), W, hip_device=-1, install_batch=b))
+    with pytest.raises(bsr.BsrError) as e:
+        bsr.bsr_ctx_create(layout(limit), 0, hip_device=-1)      # whole-plan mode: batch 32
+    assert e.value.code == bsr.BSR_E_ARG
+
+
 def test_put_chunks_matches_put_chunk_and_keeps_a_prefix_contiguous():
     """Bulk insertion: same entries and tags as one put per chunk; the chunks
     of one call sit in consecutive arena blocks; all or nothing when full."""
