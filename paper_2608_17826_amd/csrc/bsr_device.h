@@ -3,6 +3,7 @@
 // include/bsr.h.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include <hip/hip_runtime_api.h>
@@ -19,15 +20,25 @@ namespace bsr {
 #endif
 
 #ifndef BSR_INSTALL_THREADS
-#define BSR_INSTALL_THREADS 256
+#define BSR_INSTALL_THREADS 128
+#endif
+#ifndef BSR_INSTALL_WG_PER_CU
+#define BSR_INSTALL_WG_PER_CU 4
 #endif
 
 constexpr int kInstallThreads = BSR_INSTALL_THREADS;  // wave64 multiples
 constexpr int kInstallWaves = kInstallThreads / 64;
 // contiguous segments are cut into equal pieces of at most this many bytes,
-// each a multiple of 4 KiB (one 16-byte vector per thread per 4 KiB)
+// each a multiple of kPieceAlign (one 16-byte vector per thread)
 constexpr uint32_t kMaxPieceBytes = BSR_MAX_PIECE_BYTES;
 constexpr uint32_t kPieceAlign = 16 * kInstallThreads;
+// Install workgroups resident per CU.  Each holds one piece (8 KiB) of loads
+// in flight, so four keep 32 KiB per CU in flight.  The install is a mixed
+// read + write stream to scattered destinations; HBM moves it fastest with
+// that much in flight, not with the most the CU can hold (a full CU keeps
+// twice as much queued and runs about 4% slower).  The limit is applied by
+// sizing each workgroup's dynamic LDS to 1/4 of the CU's.
+constexpr uint32_t kInstallWgPerCu = BSR_INSTALL_WG_PER_CU;
 // planar pieces (whole tokens) are staged through LDS up to this size
 constexpr uint32_t kLdsCapBytes = BSR_PLANAR_PIECE_BYTES;
 
@@ -59,7 +70,22 @@ inline FastDiv make_fastdiv(uint32_t d) {
   return FastDiv{d, static_cast<uint32_t>(m), l < 1 ? l : 1u, l > 1 ? l - 1 : 0u};
 }
 
-// Per-group geometry of one install launch.
+// The same division packed for the install kernel: the multiplier and both
+// shifts in two words (s = s1 | s2 << 8).
+struct PackedDiv {
+  uint32_t m, s;
+};
+
+inline PackedDiv pack_fastdiv(const FastDiv& f) { return PackedDiv{f.m, f.s1 | (f.s2 << 8)}; }
+
+#if defined(__HIP__)
+__device__ __forceinline__ uint32_t packed_div(uint32_t m, uint32_t s, uint32_t n) {
+  const uint32_t t = static_cast<uint32_t>((static_cast<uint64_t>(m) * n) >> 32);
+  return (t + ((n - t) >> (s & 0xffu))) >> (s >> 8);
+}
+#endif
+
+// Per-group geometry of a layout, without request pointers (host side).
 struct GroupGeom {
   uint32_t block_tokens;
   uint32_t n_tensors;
@@ -71,35 +97,72 @@ struct GroupGeom {
   uint32_t pieces_per_seg;  // workgroups per (tensor, block) segment
   uint32_t piece_bytes;     // CONTIG: bytes per piece (multiple of 16)
   uint32_t piece_tokens;    // PLANAR: tokens per piece
-  uint32_t pool_blocks;
-  uint32_t n_blocks;
-  const int32_t* block_table;
-  uint8_t* const* tensor_bases;
   FastDiv div_pieces;       // by pieces_per_seg
   FastDiv div_segs;         // by segs_per_chunk
   FastDiv div_per_chunk;    // by the group's workgroups per chunk
   FastDiv div_block;        // by block_tokens
 };
 
-struct InstallParams {
-  const uint8_t* ring;
-  uint64_t slot_bytes;
-  uint32_t window;          // W (slots in the ring)
-  FastDiv div_window;       // by W
-  uint32_t chunk_tokens;
-  uint32_t n_groups;
+// Install kernel arguments.  A wave needs all of this before it can address
+// its piece, so the kernel reads the head and then its group's record each
+// as two 64-byte scalar loads issued together: two dependent rounds of
+// argument reads in all.  Word positions are fixed by the static_asserts.
+struct InstallHead {
+  // words 0-15
   uint32_t n_chunks;        // chunks in this launch (<= BSR_MAX_INSTALL_BATCH)
   uint32_t first_chunk;     // global index of the launch's first chunk
+  uint32_t chunk_tokens;
+  uint32_t window;          // W (slots in the ring)
+  PackedDiv div_window;     // by W
+  uint32_t n_groups;
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
-  uint32_t wg_start[BSR_MAX_GROUPS + 1];  // prefix of workgroups per group within a chunk
-  uint32_t lds_bytes;       // dynamic LDS of this launch
-  // Dispatch order: workgroups are issued group by group (slowest pieces
-  // first, so the launch's tail is made of the shortest pieces); within a
-  // group, chunk by chunk.  Tag partials keep their chunk-major slot.
-  uint32_t order[BSR_MAX_GROUPS];
-  GroupGeom g[BSR_MAX_GROUPS];
-  TagPair* partials;        // [n_chunks * wg_per_chunk * kInstallWaves], one per wave
+  // Workgroups are issued group by group (planar first, then by descending
+  // piece size, so the launch's tail is made of the shortest pieces); within
+  // a group, chunk by chunk.  order_prefix[o] is the number of workgroups
+  // per chunk of the groups before dispatch position o; a launch of n chunks
+  // starts position o at n * order_prefix[o].  Positions past the last group
+  // hold the total, which no workgroup index reaches.
+  uint32_t order_prefix[BSR_MAX_GROUPS];
+  // words 16-31
+  const uint8_t* ring;
+  uint64_t slot_bytes;
   const bsr_dev_status* status;
+  TagPair* partials;        // [n_chunks * wg_per_chunk * kInstallWaves], one per wave, chunk-major
+  uint32_t lds_bytes;       // dynamic LDS of this launch
+  uint32_t pad[7];
+};
+
+struct InstallGroup {
+  // words 0-15
+  uint32_t per_chunk;       // workgroups per chunk of this group
+  uint32_t wg_start;        // offset of the group's workgroups inside a chunk's tag partial slots
+  PackedDiv div_per_chunk;
+  PackedDiv div_pieces;
+  PackedDiv div_segs;
+  PackedDiv div_block;
+  uint32_t pieces_per_seg;
+  uint32_t segs_per_chunk;
+  uint32_t block_tokens;
+  uint32_t record_bytes;
+  uint32_t staged_off;
+  uint32_t piece;           // CONTIG: bytes per piece; PLANAR: tokens per piece
+  // words 16-31
+  uint32_t kind;
+  uint32_t split_bytes;
+  uint32_t n_blocks;        // entries of the block table
+  uint32_t pool_blocks;
+  const int32_t* block_table;
+  uint8_t* const* tensor_bases;
+  uint32_t group;           // index of the group in the layout
+  uint32_t pad[7];
+};
+
+static_assert(sizeof(InstallHead) == 128 && sizeof(InstallGroup) == 128, "two 64-byte scalar loads each");
+static_assert(offsetof(InstallHead, ring) == 64 && offsetof(InstallGroup, kind) == 64, "second halves start at word 16");
+
+struct InstallParams {
+  InstallHead h;
+  InstallGroup g[BSR_MAX_GROUPS];  // in dispatch order
 };
 
 // Device words the verify kernel uses across workgroups (library-owned,

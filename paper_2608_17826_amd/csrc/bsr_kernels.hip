@@ -28,7 +28,7 @@
 #include "bsr_device.h"
 
 #ifndef BSR_UNROLL
-#define BSR_UNROLL 2    // 16-byte vectors per thread of a contiguous piece
+#define BSR_UNROLL 4    // 16-byte vectors per thread of a contiguous piece
 #endif
 #ifndef BSR_NT_LOAD
 #define BSR_NT_LOAD 1   // staged chunks are read once: non-temporal loads
@@ -42,22 +42,65 @@ namespace bsr {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Ring and pool pointers are rebuilt from argument words and from tensor
+// bases read out of device memory, so the compiler cannot tell that they
+// point to global memory; every access goes through an explicit global
+// pointer (global rather than flat instructions, which would also count
+// against the LDS wait counter).
+template <typename T>
+__device__ __forceinline__ __attribute__((address_space(1))) T* global_ptr(T* p) {
+  return (__attribute__((address_space(1))) T*)(p);
+}
+
 template <typename T>
 __device__ __forceinline__ T ld_stream(const T* p) {
 #if BSR_NT_LOAD
-  return __builtin_nontemporal_load(p);
+  return __builtin_nontemporal_load(global_ptr(p));
 #else
-  return *p;
+  return *global_ptr(p);
 #endif
 }
 
 template <typename T>
 __device__ __forceinline__ void st_stream(T v, T* p) {
 #if BSR_NT_STORE
-  __builtin_nontemporal_store(v, p);
+  __builtin_nontemporal_store(v, global_ptr(p));
 #else
-  *p = v;
+  *global_ptr(p) = v;
 #endif
+}
+
+// The install's loads are issued explicitly, in program order, and waited
+// for once: a piece's data loads, then its metadata load, then one wait for
+// all of them.  Left to itself the compiler sinks the data loads below the
+// metadata check (into the branch that stores them), which turns one memory
+// round trip into two.  Vector memory loads complete in order, so an explicit
+// wait for zero outstanding loads is correct whatever the compiler issued
+// around them.
+__device__ __forceinline__ u32x4 issue_load_stream(const u32x4* p) {
+  u32x4 v;
+#if BSR_NT_LOAD
+  asm volatile("global_load_dwordx4 %0, %1, off nt" : "=v"(v) : "v"(p) : "memory");
+#else
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+#endif
+  return v;
+}
+
+__device__ __forceinline__ uint32_t issue_load_word(const uint32_t* p) {
+  uint32_t v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+
+// Wait for every issued load; each loaded register is tied to the wait so
+// that no use of it can be scheduled above it.
+template <int N>
+__device__ __forceinline__ void wait_loads(u32x4 (&v)[N], uint32_t& w) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int u = 0; u < N; ++u) asm volatile("" : "+v"(v[u]));
+  asm volatile("" : "+v"(w));
 }
 
 __device__ __forceinline__ void fold(const u32x4 v, uint32_t& s, uint32_t& x) {
@@ -65,16 +108,38 @@ __device__ __forceinline__ void fold(const u32x4 v, uint32_t& s, uint32_t& x) {
   x ^= (v.x ^ v.y) ^ (v.z ^ v.w);
 }
 
+// Wave-wide sum and XOR of a per-lane word, returned as a wave-uniform value.
+// Within each 16-lane row, lanes exchange with DPP moves (quad swaps 1 and 2,
+// then the mirrored half-row and row), so every lane of a row holds the row's
+// total; the four row totals are then read out of lanes 0, 16, 32 and 48.
+// No LDS traffic: the tag costs a few VALU cycles per wave.
+template <int kCtrl>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), kCtrl, 0xF, 0xF, false));
+}
+constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppRowMirror = 0x140;  // lane i of a row reads lane 15 - i
+constexpr int kDppHalfMirror = 0x141; // lane i of a half-row reads lane 7 - i
+
+__device__ __forceinline__ uint32_t row_lane(uint32_t v, int lane) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), lane));
+}
+
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp<kDppQuadSwap1>(v);
+  v += dpp<kDppQuadSwap2>(v);
+  v += dpp<kDppHalfMirror>(v);
+  v += dpp<kDppRowMirror>(v);
+  return (row_lane(v, 0) + row_lane(v, 16)) + (row_lane(v, 32) + row_lane(v, 48));
 }
 
 __device__ __forceinline__ uint32_t wave_xor(uint32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v ^= __shfl_xor(v, o, 64);
-  return v;
+  v ^= dpp<kDppQuadSwap1>(v);
+  v ^= dpp<kDppQuadSwap2>(v);
+  v ^= dpp<kDppHalfMirror>(v);
+  v ^= dpp<kDppRowMirror>(v);
+  return (row_lane(v, 0) ^ row_lane(v, 16)) ^ (row_lane(v, 32) ^ row_lane(v, 48));
 }
 
 // ---------------------------------------------------------------------------
@@ -87,10 +152,10 @@ __device__ __forceinline__ void copy_words(const uint8_t* __restrict__ src, uint
   uint32_t* d1 = reinterpret_cast<uint32_t*>(dst);
   const uint32_t nw = len >> 2;
   for (uint32_t i = tid; i < nw; i += kInstallThreads) {
-    const uint32_t w = s1[i];
+    const uint32_t w = *global_ptr(s1 + i);
     s += w;
     x ^= w;
-    d1[i] = w;
+    *global_ptr(d1 + i) = w;
   }
 }
 
@@ -100,6 +165,7 @@ __device__ __forceinline__ void copy_words(const uint8_t* __restrict__ src, uint
 // o*sp, plane 2 the remaining r-sp bytes at B*sp + o*(r-sp).
 // ---------------------------------------------------------------------------
 constexpr uint32_t kPlanarVecs = (kLdsCapBytes + kPieceAlign - 1) / kPieceAlign;  // vectors per thread
+static_assert(kPlanarVecs * kPieceAlign >= kLdsCapBytes, "a planar piece of kLdsCapBytes fits the registers");
 
 // Fast path, second half: the piece's words are in registers (v); stage them
 // in LDS, then write plane 1 with 16-byte stores and plane 2 with 4-byte stores.
@@ -138,7 +204,7 @@ __device__ __forceinline__ void planar_from_regs(const u32x4 (&v)[kPlanarVecs], 
   for (uint32_t i = tid; i < n2; i += kInstallThreads) {
     const uint32_t u = i / w2;
     const uint32_t wi = i - u * w2;
-    d2[i] = l1[((u * r + sp) >> 2) + wi];
+    st_stream(l1[((u * r + sp) >> 2) + wi], d2 + i);
   }
 }
 
@@ -153,14 +219,72 @@ __device__ __forceinline__ void planar_words(const uint8_t* __restrict__ src, ui
   for (uint32_t i = tid; i < nw; i += kInstallThreads) {
     const uint32_t u = i / rw;
     const uint32_t wi = i - u * rw;
-    const uint32_t w = s1[i];
+    const uint32_t w = *global_ptr(s1 + i);
     s += w;
     x ^= w;
     if (wi < sw)
-      d1[u * sw + wi] = w;
+      *global_ptr(d1 + u * sw + wi) = w;
     else
-      d2[u * (rw - sw) + (wi - sw)] = w;
+      *global_ptr(d2 + u * (rw - sw) + (wi - sw)) = w;
   }
+}
+
+// Destination metadata of one segment and the request's status words,
+// fetched by one vector load per wave issued right after the piece's data
+// loads: lane 0 reads the destination block id, lanes 1-2 the two halves of
+// the tensor base, lane 3 the fail word and lanes 4.. the per-group q_g.  The
+// data and the metadata then arrive in one memory round trip, and the values
+// are broadcast from their lanes.
+struct SegMeta {
+  int32_t block;
+  uint8_t* tensor_base;
+  bool past_prefix;  // a failure is recorded, or some group is invalid
+};
+
+__device__ __forceinline__ const uint32_t* meta_addr(const bsr_dev_status* status, const int32_t* block_table,
+                                                     uint8_t* const* tensor_bases, uint64_t k, uint32_t t,
+                                                     uint32_t lane) {
+  const uint32_t* st = reinterpret_cast<const uint32_t*>(status);
+  const uint32_t* a = st;  // lane 3 and every lane past the q words: the fail word
+  if (lane == 0) a = reinterpret_cast<const uint32_t*>(block_table + k);
+  if (lane == 1 || lane == 2) a = reinterpret_cast<const uint32_t*>(tensor_bases + t) + (lane - 1);
+  if (lane >= 4 && lane < 4 + BSR_MAX_GROUPS) a = st + 2 + (lane - 4);  // q[lane - 4]
+  return a;
+}
+
+__device__ __forceinline__ SegMeta broadcast_meta(uint32_t w, uint32_t lane, uint32_t n_groups) {
+  SegMeta m;
+  m.block = static_cast<int32_t>(row_lane(w, 0));
+  // both halves widened from uint32_t: the builtin returns int, and a
+  // widened int would sign-extend a low half whose bit 31 is set
+  const uint64_t lo = row_lane(w, 1), hi = row_lane(w, 2);
+  m.tensor_base = reinterpret_cast<uint8_t*>(lo | (hi << 32));
+  // Prefix check: a failure recorded by an earlier chunk, or an invalid
+  // group, puts this chunk past the valid prefix.  Nothing writes the status
+  // words while installs run, so every wave sees the same values and the
+  // whole workgroup agrees.
+  const bool bad = (lane == 3 && w != 0) || (lane >= 4 && lane < 4 + n_groups && w == 0);
+  m.past_prefix = __ballot(bad) != 0ull;
+  return m;
+}
+
+// 128 bytes of kernel arguments as two 64-byte vectors: each becomes one
+// scalar load, and both are issued before either is waited for.
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+template <typename T>
+union ArgWords {
+  u32x16 v[2];
+  T s;
+};
+
+template <typename T>
+__device__ __forceinline__ T load_args(const T* src) {
+  static_assert(sizeof(T) == sizeof(u32x16) * 2, "argument blocks are 128 bytes");
+  ArgWords<T> w;
+  const u32x16* v = reinterpret_cast<const u32x16*>(src);
+  w.v[0] = v[0];
+  w.v[1] = v[1];
+  return w.s;
 }
 
 __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams p) {
@@ -168,78 +292,74 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
 
   const uint32_t tid = threadIdx.x;
   const uint32_t lane = tid & 63;
-  uint32_t rem = blockIdx.x;
-  // work index -> (group, chunk, piece within the chunk's group range)
-  uint32_t oi = 0, gi = p.order[0];
-  for (;;) {
-    const uint32_t n = (p.wg_start[gi + 1] - p.wg_start[gi]) * p.n_chunks;
-    if (rem < n || oi + 1 == p.n_groups) break;
-    rem -= n;
-    gi = p.order[++oi];
+  const InstallHead H = load_args(&p.h);
+  // work index -> dispatch position (the group), then (chunk, piece within
+  // the chunk's group range)
+  const uint32_t bid = blockIdx.x;
+  uint32_t oi = 0, base = 0;
+#pragma unroll
+  for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) {
+    const uint32_t start = H.n_chunks * H.order_prefix[q];
+    const bool in = bid >= start;  // the prefix is increasing: the last start at or below bid wins
+    oi = in ? q : oi;
+    base = in ? start : base;
   }
-  const GroupGeom& G = p.g[gi];
-  const uint32_t per_chunk = p.wg_start[gi + 1] - p.wg_start[gi];
-  const uint32_t c = G.div_per_chunk.div(rem);
-  rem -= c * per_chunk;
-  const uint32_t wg = c * p.wg_per_chunk + p.wg_start[gi] + rem;  // chunk-major slot of the tag partials
+  const InstallGroup G = load_args(&p.g[oi]);
+  uint32_t rem = bid - base;
+  const uint32_t c = packed_div(G.div_per_chunk.m, G.div_per_chunk.s, rem);
+  rem -= c * G.per_chunk;
+  const uint32_t wg = c * H.wg_per_chunk + G.wg_start + rem;  // chunk-major slot of the tag partials
 
-  const uint32_t r1 = G.div_pieces.div(rem);
+  const uint32_t r1 = packed_div(G.div_pieces.m, G.div_pieces.s, rem);
   const uint32_t piece = rem - r1 * G.pieces_per_seg;
-  const uint32_t t = G.div_segs.div(r1);
+  const uint32_t t = packed_div(G.div_segs.m, G.div_segs.s, r1);
   const uint32_t j = r1 - t * G.segs_per_chunk;
 
-  const uint32_t chunk = p.first_chunk + c;
-  const uint32_t slot = chunk - p.div_window.div(chunk) * p.window;
-  const uint64_t C = p.chunk_tokens, B = G.block_tokens;
-  const uint32_t tok0_32 = chunk * p.chunk_tokens;  // the bound prefix has < 2^32 tokens
+  const uint32_t chunk = H.first_chunk + c;
+  const uint32_t slot = chunk - packed_div(H.div_window.m, H.div_window.s, chunk) * H.window;
+  const uint64_t C = H.chunk_tokens, B = G.block_tokens;
+  const uint32_t tok0_32 = chunk * H.chunk_tokens;  // the bound prefix has < 2^32 tokens
   const uint64_t tok0 = tok0_32;
-  const uint64_t k = G.div_block.div(tok0_32) + j;  // request block index
+  const uint64_t k = packed_div(G.div_block.m, G.div_block.s, tok0_32) + j;  // request block index
   const uint64_t blo = k * B;
   const uint64_t lo = tok0 > blo ? tok0 : blo;
   const uint64_t hi = (tok0 + C) < (blo + B) ? (tok0 + C) : (blo + B);
 
   uint32_t s = 0, x = 0;
   if (lo < hi && k < G.n_blocks) {
-    // Metadata loads first (status words, destination block id, tensor base);
-    // they resolve while the staged bytes are loaded: the source address
-    // depends on none of them.
-    bool bad = false;
-    if (lane == 0)
-      bad = p.status->fail != 0;
-    else if (lane <= p.n_groups)
-      bad = p.status->q[lane - 1] == 0;
-    const int32_t b = G.block_table[k];
-    uint8_t* const tbase = G.tensor_bases[t];
-
     const uint32_t r = G.record_bytes;
     const uint32_t m = static_cast<uint32_t>(hi - lo);
     const uint32_t q0 = static_cast<uint32_t>(lo - tok0);
     const uint32_t o0 = static_cast<uint32_t>(lo - blo);
-    const uint8_t* src = p.ring + static_cast<uint64_t>(slot) * p.slot_bytes + G.staged_off +
+    const uint8_t* src = H.ring + static_cast<uint64_t>(slot) * H.slot_bytes + G.staged_off +
                          (static_cast<uint64_t>(t) * C + q0) * r;
     if (G.kind == BSR_KIND_CONTIG) {
       const uint32_t seg = m * r;
-      const uint32_t off = piece * G.piece_bytes;
-      const uint32_t len = off < seg ? ((seg - off) < G.piece_bytes ? (seg - off) : G.piece_bytes) : 0;
+      const uint32_t off = piece * G.piece;
+      const uint32_t len = off < seg ? ((seg - off) < G.piece ? (seg - off) : G.piece) : 0;
       const uint8_t* sp = src + off;
       const uint32_t nvec = len >> 4;
       constexpr uint32_t U = BSR_UNROLL;
       static_assert(kMaxPieceBytes <= U * kPieceAlign, "a contiguous piece must fit one unrolled pass");
-      const bool one_pass = ((reinterpret_cast<uintptr_t>(sp) | len) & 15u) == 0;
+      const bool one_pass = ((reinterpret_cast<uintptr_t>(sp) | len) & 15u) == 0 && nvec != 0;
+      // Every lane loads, with no branch around the loads (a branch would
+      // make the compiler wait for them where its paths join, before the
+      // metadata load is issued): lanes past the piece's end reload its last
+      // vector, and a piece that takes the word path loads the ring's first
+      // vector instead, a valid aligned address whose value is not used.
+      const u32x4* s4 = reinterpret_cast<const u32x4*>(one_pass ? sp : H.ring);
+      const uint32_t last = one_pass ? nvec - 1 : 0;
       u32x4 v[U];
-      if (one_pass) {
 #pragma unroll
-        for (uint32_t u = 0; u < U; ++u) {
-          const uint32_t i = u * kInstallThreads + tid;
-          if (i < nvec) v[u] = ld_stream(reinterpret_cast<const u32x4*>(sp) + i);
-        }
+      for (uint32_t u = 0; u < U; ++u) {
+        const uint32_t i = u * kInstallThreads + tid;
+        v[u] = issue_load_stream(s4 + (i < last ? i : last));
       }
-      // Wave-level prefix check: a failure recorded by an earlier chunk (or an
-      // invalid group) puts this chunk past the valid prefix; every wave
-      // ballots the same words, so the whole workgroup agrees.
-      const bool skip = __ballot(bad) != 0ull;
-      if (!skip && b >= 0 && static_cast<uint32_t>(b) < G.pool_blocks && len) {
-        uint8_t* dp = tbase + static_cast<uint64_t>(b) * B * r + static_cast<uint64_t>(o0) * r + off;
+      uint32_t mw = issue_load_word(meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
+      wait_loads(v, mw);
+      const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
+      if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && len) {
+        uint8_t* dp = md.tensor_base + static_cast<uint64_t>(md.block) * B * r + static_cast<uint64_t>(o0) * r + off;
         if (one_pass && (reinterpret_cast<uintptr_t>(dp) & 15u) == 0) {
           u32x4* d4 = reinterpret_cast<u32x4*>(dp);
 #pragma unroll
@@ -256,23 +376,28 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       }
     } else {
       const uint32_t sp = G.split_bytes;
-      const uint32_t u0 = piece * G.piece_tokens;
-      const uint32_t mu = u0 < m ? ((m - u0) < G.piece_tokens ? (m - u0) : G.piece_tokens) : 0;
+      const uint32_t u0 = piece * G.piece;
+      const uint32_t mu = u0 < m ? ((m - u0) < G.piece ? (m - u0) : G.piece) : 0;
       const uint8_t* psrc = src + static_cast<uint64_t>(u0) * r;
       const uint32_t bytes = mu * r;
       const uint32_t nvec = bytes >> 4;
-      const bool src_ok = ((reinterpret_cast<uintptr_t>(psrc) | bytes | sp) & 15u) == 0 && bytes <= p.lds_bytes;
+      const bool src_ok =
+          ((reinterpret_cast<uintptr_t>(psrc) | bytes | sp) & 15u) == 0 && bytes <= kLdsCapBytes &&
+          bytes <= H.lds_bytes && nvec != 0;  // the piece fits the registers (v) and the LDS
+      // unconditional loads, as for contiguous pieces
+      const u32x4* s4 = reinterpret_cast<const u32x4*>(src_ok ? psrc : H.ring);
+      const uint32_t last = src_ok ? nvec - 1 : 0;
       u32x4 v[kPlanarVecs];
-      if (src_ok) {
 #pragma unroll
-        for (uint32_t u = 0; u < kPlanarVecs; ++u) {
-          const uint32_t i = u * kInstallThreads + tid;
-          if (i < nvec) v[u] = ld_stream(reinterpret_cast<const u32x4*>(psrc) + i);
-        }
+      for (uint32_t u = 0; u < kPlanarVecs; ++u) {
+        const uint32_t i = u * kInstallThreads + tid;
+        v[u] = issue_load_stream(s4 + (i < last ? i : last));
       }
-      const bool skip = __ballot(bad) != 0ull;
-      if (!skip && b >= 0 && static_cast<uint32_t>(b) < G.pool_blocks && mu) {
-        uint8_t* blk = tbase + static_cast<uint64_t>(b) * B * r;
+      uint32_t mw = issue_load_word(meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
+      wait_loads(v, mw);
+      const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
+      if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && mu) {
+        uint8_t* blk = md.tensor_base + static_cast<uint64_t>(md.block) * B * r;
         uint8_t* dst1 = blk + static_cast<uint64_t>(o0 + u0) * sp;
         uint8_t* dst2 = blk + B * sp + static_cast<uint64_t>(o0 + u0) * (r - sp);
         if (src_ok && ((reinterpret_cast<uintptr_t>(dst1) & 15u) | (reinterpret_cast<uintptr_t>(dst2) & 3u)) == 0)
@@ -286,7 +411,11 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   // one tag partial per wave
   s = wave_sum(s);
   x = wave_xor(x);
-  if (lane == 0) p.partials[wg * kInstallWaves + (tid >> 6)] = TagPair{s, x};
+  // TagPair {sum, xor} as one little-endian 8-byte word
+  static_assert(sizeof(TagPair) == 8 && offsetof(TagPair, x) == 4, "sum in the low word");
+  if (lane == 0)
+    *global_ptr(reinterpret_cast<uint64_t*>(H.partials) + wg * kInstallWaves + (tid >> 6)) =
+        static_cast<uint64_t>(s) | (static_cast<uint64_t>(x) << 32);
 }
 
 // One workgroup per (chunk, group) of the launch reduces that entry's wave
@@ -425,9 +554,9 @@ hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStre
                           hipEvent_t stop) {
   if (start && stop) {
     // the events are stamped by the kernel's own dispatch (no marker packets)
-    hipExtLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.lds_bytes, s, start, stop, 0, p);
+    hipExtLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.h.lds_bytes, s, start, stop, 0, p);
   } else {
-    hipLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.lds_bytes, s, p);
+    hipLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.h.lds_bytes, s, p);
   }
   return hipGetLastError();
 }

@@ -152,6 +152,7 @@ struct Geometry {
   uint32_t wg_per_chunk = 0;
   uint32_t lds_bytes = 0;
   uint32_t order[BSR_MAX_GROUPS]{};  // install dispatch order of the groups
+  uint32_t order_prefix[BSR_MAX_GROUPS + 1]{};  // workgroups per chunk before each position of that order
 };
 
 int check_layout(const bsr_layout* L) {
@@ -240,6 +241,12 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
     return q.kind == BSR_KIND_PLANAR ? (1ull << 40) : q.piece_bytes;
   };
   std::stable_sort(G->order, G->order + L->n_groups, [&](uint32_t a, uint32_t b) { return cost(a) > cost(b); });
+  uint32_t acc = 0;
+  for (uint32_t o = 0; o < L->n_groups; ++o) {
+    G->order_prefix[o] = acc;
+    acc += G->wg_start[G->order[o] + 1] - G->wg_start[G->order[o]];
+  }
+  for (uint32_t o = L->n_groups; o <= BSR_MAX_GROUPS; ++o) G->order_prefix[o] = acc;
   G->slot_bytes = off;
   G->chunk_payload = 0;
   for (uint32_t g = 0; g < L->n_groups; ++g) G->chunk_payload += G->payload[g];
@@ -455,15 +462,15 @@ int flush_batch(bsr_ctx* c, Session& s) {
   if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
 
   InstallParams ip = s.ip;
-  ip.n_chunks = static_cast<uint32_t>(chunks.size());
-  ip.first_chunk = chunks.front();
+  ip.h.n_chunks = static_cast<uint32_t>(chunks.size());
+  ip.h.first_chunk = chunks.front();
   hipEvent_t t0 = nullptr, t1 = nullptr;
   if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
     t1 = take_timing_event(c);
     if (!t0 || !t1) t0 = t1 = nullptr;
   }
-  if ((rc = hip_check(bsr::launch_install(ip, ip.n_chunks * ip.wg_per_chunk, s.compute, t0, t1), "install launch"))) {
+  if ((rc = hip_check(bsr::launch_install(ip, ip.h.n_chunks * ip.h.wg_per_chunk, s.compute, t0, t1), "install launch"))) {
     if (t0) c->timing_pool.push_back(t0);
     if (t1) c->timing_pool.push_back(t1);
     return rc;
@@ -473,11 +480,11 @@ int flush_batch(bsr_ctx* c, Session& s) {
   vp.partials = r.partials;
   vp.status = s.status;
   vp.aux = r.verify_aux;
-  vp.n_chunks = ip.n_chunks;
-  vp.first_chunk = ip.first_chunk;
+  vp.n_chunks = ip.h.n_chunks;
+  vp.first_chunk = ip.h.first_chunk;
   vp.n_groups = c->geo.L.n_groups;
-  vp.wg_per_chunk = ip.wg_per_chunk;
-  std::memcpy(vp.wg_start, ip.wg_start, sizeof vp.wg_start);
+  vp.wg_per_chunk = ip.h.wg_per_chunk;
+  std::memcpy(vp.wg_start, c->geo.wg_start, sizeof vp.wg_start);
   for (size_t i = 0; i < chunks.size(); ++i)
     for (uint32_t g = 0; g < BSR_MAX_GROUPS; ++g) vp.expected[i][g] = tags[i][g];
   if ((rc = hip_check(bsr::launch_verify(vp, s.compute), "verify launch"))) return rc;
@@ -667,6 +674,24 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
       delete c;
       return rc;
     }
+    // occupancy of the install kernel: each workgroup takes 1/kInstallWgPerCu
+    // of the CU's LDS (at least what its planar pieces need)
+    int lds_per_cu = 0, lds_per_block = 0;
+    if ((rc = hip_check(hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device),
+                        "hipDeviceGetAttribute")) ||
+        (rc = hip_check(hipDeviceGetAttribute(&lds_per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device),
+                        "hipDeviceGetAttribute"))) {
+      delete c;
+      return rc;
+    }
+    const uint32_t share = std::min<uint32_t>(static_cast<uint32_t>(lds_per_cu) / bsr::kInstallWgPerCu / 256 * 256,
+                                              static_cast<uint32_t>(lds_per_block));
+    if (c->geo.lds_bytes > static_cast<uint32_t>(lds_per_block)) {
+      delete c;
+      return fail_with(BSR_E_ARG, "planar pieces need %u B of LDS, the device has %d per workgroup", c->geo.lds_bytes,
+                       lds_per_block);
+    }
+    c->geo.lds_bytes = std::max(c->geo.lds_bytes, share);
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
     c->aux_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
     // event ring: the copy of chunk i waits for the release of chunk i - W,
@@ -982,17 +1007,16 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   fp.exposed_if_valid = static_cast<uint64_t>(n_hit) * C;
   const bool trusted = (c->cfg.flags & BSR_FLAG_TRUSTED_TABLES) != 0;
   InstallParams ip{};
-  ip.ring = static_cast<const uint8_t*>(staging);
-  ip.slot_bytes = c->geo.slot_bytes;
-  ip.window = window;
-  ip.div_window = bsr::make_fastdiv(window);
-  ip.chunk_tokens = C;
-  ip.n_groups = G;
-  ip.wg_per_chunk = c->geo.wg_per_chunk;
-  std::memcpy(ip.wg_start, c->geo.wg_start, sizeof ip.wg_start);
-  std::memcpy(ip.order, c->geo.order, sizeof ip.order);
-  ip.lds_bytes = c->geo.lds_bytes;
-  ip.status = status;
+  ip.h.ring = static_cast<const uint8_t*>(staging);
+  ip.h.slot_bytes = c->geo.slot_bytes;
+  ip.h.window = window;
+  ip.h.div_window = bsr::pack_fastdiv(bsr::make_fastdiv(window));
+  ip.h.chunk_tokens = C;
+  ip.h.n_groups = G;
+  ip.h.wg_per_chunk = c->geo.wg_per_chunk;
+  for (uint32_t o = 0; o < BSR_MAX_GROUPS; ++o) ip.h.order_prefix[o] = c->geo.order_prefix[o];
+  ip.h.lds_bytes = c->geo.lds_bytes;
+  ip.h.status = status;
   uint32_t total = 0;
   std::vector<int32_t> bt;
   for (uint32_t g = 0; g < G; ++g) {
@@ -1018,12 +1042,30 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
         if (seen[b]++) return fail_with(BSR_E_ARG, "group %u: block %d appears twice in the prefix", g, b);
       }
     }
-    GroupGeom q = c->geo.gg[g];
-    q.pool_blocks = d.pool_blocks;
-    q.n_blocks = d.n_blocks;
-    q.block_table = d.block_table;
-    q.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
-    ip.g[g] = q;
+    // the group's record sits at its dispatch position
+    uint32_t pos = 0;
+    while (c->geo.order[pos] != g) ++pos;
+    const GroupGeom& q = c->geo.gg[g];
+    bsr::InstallGroup& ig = ip.g[pos];
+    ig.per_chunk = c->geo.wg_start[g + 1] - c->geo.wg_start[g];
+    ig.wg_start = c->geo.wg_start[g];
+    ig.div_per_chunk = bsr::pack_fastdiv(q.div_per_chunk);
+    ig.div_pieces = bsr::pack_fastdiv(q.div_pieces);
+    ig.div_segs = bsr::pack_fastdiv(q.div_segs);
+    ig.div_block = bsr::pack_fastdiv(q.div_block);
+    ig.pieces_per_seg = q.pieces_per_seg;
+    ig.segs_per_chunk = q.segs_per_chunk;
+    ig.block_tokens = q.block_tokens;
+    ig.record_bytes = q.record_bytes;
+    ig.staged_off = q.staged_off;
+    ig.piece = q.kind == BSR_KIND_CONTIG ? q.piece_bytes : q.piece_tokens;
+    ig.kind = q.kind;
+    ig.split_bytes = q.split_bytes;
+    ig.n_blocks = d.n_blocks;
+    ig.pool_blocks = d.pool_blocks;
+    ig.block_table = d.block_table;
+    ig.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
+    ig.group = g;
     fp.g[g] = bsr::GroupValid{d.block_table, d.valid, static_cast<uint32_t>(nreq), d.pool_blocks, B, 0};
     total += static_cast<uint32_t>(nreq);
   }
@@ -1072,7 +1114,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   }
   SessionRes& res = c->res[slot_res];
   fp.verify_aux = res.verify_aux;
-  ip.partials = res.partials;
+  ip.h.partials = res.partials;
 
   if (c->W == 0) {
     // whole-plan mode: one event pair per install batch of the plan

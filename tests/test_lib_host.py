@@ -231,11 +231,12 @@ def test_admission_config_errors_and_defaults():
 
 def test_install_grid_limit():
     """One install launch runs install_batch x (workgroups per chunk) workgroups
-    of 256 threads; a layout and batch whose grid would pass 2^32 - 1
-    work-items is refused at creation, and a smaller batch is accepted."""
+    of 128 threads (the install kernel's workgroup size); a layout and batch
+    whose grid would pass 2^32 - 1 work-items is refused at creation, and a
+    smaller batch is accepted."""
     def layout(n_tensors):   # one token per chunk and per block, 4-byte records: one workgroup per tensor
         return bsr.make_layout(1, [(1, n_tensors, 4, bsr.BSR_KIND_CONTIG, 0)])
-    limit = (1 << 32) // (32 * 256)          # 524,288 tensors at the automatic batch of 32 (W = 64)
+    limit = (1 << 32) // (32 * 128)          # 1,048,576 tensors at the automatic batch of 32 (W = 64)
     with pytest.raises(bsr.BsrError) as e:
         bsr.bsr_ctx_create(layout(limit), 64, hip_device=-1)
     assert e.value.code == bsr.BSR_E_ARG and "grid limit" in bsr.bsr_last_error()
