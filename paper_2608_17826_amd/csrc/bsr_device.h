@@ -154,7 +154,9 @@ struct InstallGroup {
   const int32_t* block_table;
   uint8_t* const* tensor_bases;
   uint32_t group;           // index of the group in the layout
-  uint32_t pad[7];
+  PackedDiv div_p1;         // PLANAR: by plane-1 vectors per token (split_bytes / 16)
+  PackedDiv div_p2;         // PLANAR: by plane-2 words per token ((record_bytes - split_bytes) / 4)
+  uint32_t pad[3];
 };
 
 static_assert(sizeof(InstallHead) == 128 && sizeof(InstallGroup) == 128, "two 64-byte scalar loads each");

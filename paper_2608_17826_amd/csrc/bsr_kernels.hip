@@ -168,10 +168,16 @@ constexpr uint32_t kPlanarVecs = (kLdsCapBytes + kPieceAlign - 1) / kPieceAlign;
 static_assert(kPlanarVecs * kPieceAlign >= kLdsCapBytes, "a planar piece of kLdsCapBytes fits the registers");
 
 // Fast path, second half: the piece's words are in registers (v); stage them
-// in LDS, then write plane 1 with 16-byte stores and plane 2 with 4-byte stores.
+// in LDS, then write plane 1 with 16-byte stores and plane 2 with 4-byte
+// stores.  Plane 1 has fewer vectors than the piece (split < record), so it
+// fits the same per-thread count: every thread reads all its plane-1 vectors
+// out of LDS at once (indices clamped to the last, no per-lane branch) and
+// waits once, instead of once per vector.  d1/d2 are the divisions by the
+// plane-1 vectors and plane-2 words per token.
 __device__ __forceinline__ void planar_from_regs(const u32x4 (&v)[kPlanarVecs], uint32_t nvec, uint8_t* dst1,
                                                  uint8_t* dst2, uint32_t mu, uint32_t r, uint32_t sp,
-                                                 uint8_t* lds, uint32_t tid, uint32_t& s, uint32_t& x) {
+                                                 const PackedDiv d1, const PackedDiv d2, uint8_t* lds,
+                                                 uint32_t tid, uint32_t& s, uint32_t& x) {
   u32x4* l4 = reinterpret_cast<u32x4*>(lds);
 #pragma unroll
   for (uint32_t u = 0; u < kPlanarVecs; ++u) {
@@ -183,28 +189,33 @@ __device__ __forceinline__ void planar_from_regs(const u32x4 (&v)[kPlanarVecs], 
   }
   __syncthreads();
   const uint32_t* l1 = reinterpret_cast<const uint32_t*>(lds);
-  // plane 1: vector i covers token i / (sp/16), part i % (sp/16)
+  // plane 1: vector i covers token i / vpt, part i % vpt
   const uint32_t vpt = sp >> 4;
-  const uint32_t n1 = mu * vpt;
+  const uint32_t n1 = mu * vpt;  // n1 * 16 < mu * r <= kLdsCapBytes: at most kPlanarVecs per thread
+  u32x4 w[kPlanarVecs];
+#pragma unroll
+  for (uint32_t u = 0; u < kPlanarVecs; ++u) {
+    const uint32_t i0 = u * kInstallThreads + tid;
+    const uint32_t i = i0 < n1 ? i0 : n1 - 1;
+    const uint32_t tk = packed_div(d1.m, d1.s, i);
+    const uint32_t w0 = (tk * r + (i - tk * vpt) * 16) >> 2;
+    w[u].x = l1[w0];
+    w[u].y = l1[w0 + 1];
+    w[u].z = l1[w0 + 2];
+    w[u].w = l1[w0 + 3];
+  }
   u32x4* d4 = reinterpret_cast<u32x4*>(dst1);
-  for (uint32_t i = tid; i < n1; i += kInstallThreads) {
-    const uint32_t u = i / vpt;
-    const uint32_t part = i - u * vpt;
-    const uint32_t w0 = (u * r + part * 16) >> 2;
-    u32x4 w;
-    w.x = l1[w0];
-    w.y = l1[w0 + 1];
-    w.z = l1[w0 + 2];
-    w.w = l1[w0 + 3];
-    st_stream(w, d4 + i);
+#pragma unroll
+  for (uint32_t u = 0; u < kPlanarVecs; ++u) {
+    const uint32_t i = u * kInstallThreads + tid;
+    if (i < n1) st_stream(w[u], d4 + i);
   }
   const uint32_t w2 = (r - sp) >> 2;
   const uint32_t n2 = mu * w2;
-  uint32_t* d2 = reinterpret_cast<uint32_t*>(dst2);
+  uint32_t* dw = reinterpret_cast<uint32_t*>(dst2);
   for (uint32_t i = tid; i < n2; i += kInstallThreads) {
-    const uint32_t u = i / w2;
-    const uint32_t wi = i - u * w2;
-    st_stream(l1[((u * r + sp) >> 2) + wi], d2 + i);
+    const uint32_t tk = packed_div(d2.m, d2.s, i);
+    st_stream(l1[((tk * r + sp) >> 2) + (i - tk * w2)], dw + i);
   }
 }
 
@@ -401,7 +412,7 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
         uint8_t* dst1 = blk + static_cast<uint64_t>(o0 + u0) * sp;
         uint8_t* dst2 = blk + B * sp + static_cast<uint64_t>(o0 + u0) * (r - sp);
         if (src_ok && ((reinterpret_cast<uintptr_t>(dst1) & 15u) | (reinterpret_cast<uintptr_t>(dst2) & 3u)) == 0)
-          planar_from_regs(v, nvec, dst1, dst2, mu, r, sp, lds, tid, s, x);
+          planar_from_regs(v, nvec, dst1, dst2, mu, r, sp, G.div_p1, G.div_p2, lds, tid, s, x);
         else
           planar_words(psrc, dst1, dst2, mu, r, sp, tid, s, x);
       }

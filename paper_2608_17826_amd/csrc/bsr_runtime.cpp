@@ -1066,6 +1066,10 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     ig.block_table = d.block_table;
     ig.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
     ig.group = g;
+    if (q.kind == BSR_KIND_PLANAR) {
+      ig.div_p1 = bsr::pack_fastdiv(bsr::make_fastdiv(std::max(1u, q.split_bytes / 16)));
+      ig.div_p2 = bsr::pack_fastdiv(bsr::make_fastdiv((q.record_bytes - q.split_bytes) / 4));
+    }
     fp.g[g] = bsr::GroupValid{d.block_table, d.valid, static_cast<uint32_t>(nreq), d.pool_blocks, B, 0};
     total += static_cast<uint32_t>(nreq);
   }
