@@ -53,15 +53,6 @@ __device__ __forceinline__ __attribute__((address_space(1))) T* global_ptr(T* p)
 }
 
 template <typename T>
-__device__ __forceinline__ T ld_stream(const T* p) {
-#if BSR_NT_LOAD
-  return __builtin_nontemporal_load(global_ptr(p));
-#else
-  return *global_ptr(p);
-#endif
-}
-
-template <typename T>
 __device__ __forceinline__ void st_stream(T v, T* p) {
 #if BSR_NT_STORE
   __builtin_nontemporal_store(v, global_ptr(p));
@@ -70,38 +61,50 @@ __device__ __forceinline__ void st_stream(T v, T* p) {
 #endif
 }
 
-// The install's loads are issued explicitly, in program order, and waited
-// for once: a piece's data loads, then its metadata load, then one wait for
-// all of them.  Left to itself the compiler sinks the data loads below the
-// metadata check (into the branch that stores them), which turns one memory
-// round trip into two.  Vector memory loads complete in order, so an explicit
-// wait for zero outstanding loads is correct whatever the compiler issued
-// around them.
-__device__ __forceinline__ u32x4 issue_load_stream(const u32x4* p) {
-  u32x4 v;
+// The install's loads are issued explicitly: a piece's data loads, then its
+// metadata load, then one wait for all of them, in a single asm statement.
+// Left to itself the compiler sinks the data loads below the metadata check
+// (into the branch that stores them), which turns one memory round trip into
+// two.  Inside one statement the loaded registers are only defined once the
+// wait has passed, so no instruction can read them early, and early-clobber
+// outputs keep every destination apart from the addresses of later loads.
+// One burst shape per per-thread load count the kernel is built with.
 #if BSR_NT_LOAD
-  asm volatile("global_load_dwordx4 %0, %1, off nt" : "=v"(v) : "v"(p) : "memory");
+#define BSR_LDX4(d, a) "global_load_dwordx4 %" #d ", %" #a ", off nt\n\t"
 #else
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+#define BSR_LDX4(d, a) "global_load_dwordx4 %" #d ", %" #a ", off\n\t"
 #endif
-  return v;
-}
+#define BSR_LD1(d, a) "global_load_dword %" #d ", %" #a ", off\n\t"
+#define BSR_WAIT "s_waitcnt vmcnt(0)"
 
-__device__ __forceinline__ uint32_t issue_load_word(const uint32_t* p) {
-  uint32_t v;
-  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-  return v;
-}
-
-// Wait for every issued load; each loaded register is tied to the wait so
-// that no use of it can be scheduled above it.
 template <int N>
-__device__ __forceinline__ void wait_loads(u32x4 (&v)[N], uint32_t& w) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-  for (int u = 0; u < N; ++u) asm volatile("" : "+v"(v[u]));
-  asm volatile("" : "+v"(w));
-}
+struct LoadBurst;  // N 16-byte stream loads + one metadata word, waited for together
+
+template <>
+struct LoadBurst<4> {
+  static __device__ __forceinline__ void run(u32x4 (&v)[4], uint32_t& w, const u32x4* const (&a)[4],
+                                             const uint32_t* am) {
+    asm volatile(BSR_LDX4(0, 5) BSR_LDX4(1, 6) BSR_LDX4(2, 7) BSR_LDX4(3, 8) BSR_LD1(4, 9) BSR_WAIT
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(w)
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(am)
+                 : "memory");
+  }
+};
+
+template <>
+struct LoadBurst<10> {
+  static __device__ __forceinline__ void run(u32x4 (&v)[10], uint32_t& w, const u32x4* const (&a)[10],
+                                             const uint32_t* am) {
+    asm volatile(BSR_LDX4(0, 11) BSR_LDX4(1, 12) BSR_LDX4(2, 13) BSR_LDX4(3, 14) BSR_LDX4(4, 15)
+                 BSR_LDX4(5, 16) BSR_LDX4(6, 17) BSR_LDX4(7, 18) BSR_LDX4(8, 19) BSR_LDX4(9, 20)
+                 BSR_LD1(10, 21) BSR_WAIT
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]),
+                   "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9]), "=&v"(w)
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]),
+                   "v"(a[8]), "v"(a[9]), "v"(am)
+                 : "memory");
+  }
+};
 
 __device__ __forceinline__ void fold(const u32x4 v, uint32_t& s, uint32_t& x) {
   s += (v.x + v.y) + (v.z + v.w);
@@ -360,14 +363,15 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       // vector instead, a valid aligned address whose value is not used.
       const u32x4* s4 = reinterpret_cast<const u32x4*>(one_pass ? sp : H.ring);
       const uint32_t last = one_pass ? nvec - 1 : 0;
-      u32x4 v[U];
+      const u32x4* at[U];
 #pragma unroll
       for (uint32_t u = 0; u < U; ++u) {
         const uint32_t i = u * kInstallThreads + tid;
-        v[u] = issue_load_stream(s4 + (i < last ? i : last));
+        at[u] = s4 + (i < last ? i : last);
       }
-      uint32_t mw = issue_load_word(meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
-      wait_loads(v, mw);
+      u32x4 v[U];
+      uint32_t mw;
+      LoadBurst<U>::run(v, mw, at, meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
       const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
       if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && len) {
         uint8_t* dp = md.tensor_base + static_cast<uint64_t>(md.block) * B * r + static_cast<uint64_t>(o0) * r + off;
@@ -398,14 +402,15 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       // unconditional loads, as for contiguous pieces
       const u32x4* s4 = reinterpret_cast<const u32x4*>(src_ok ? psrc : H.ring);
       const uint32_t last = src_ok ? nvec - 1 : 0;
-      u32x4 v[kPlanarVecs];
+      const u32x4* at[kPlanarVecs];
 #pragma unroll
       for (uint32_t u = 0; u < kPlanarVecs; ++u) {
         const uint32_t i = u * kInstallThreads + tid;
-        v[u] = issue_load_stream(s4 + (i < last ? i : last));
+        at[u] = s4 + (i < last ? i : last);
       }
-      uint32_t mw = issue_load_word(meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
-      wait_loads(v, mw);
+      u32x4 v[kPlanarVecs];
+      uint32_t mw;
+      LoadBurst<kPlanarVecs>::run(v, mw, at, meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
       const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
       if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && mu) {
         uint8_t* blk = md.tensor_base + static_cast<uint64_t>(md.block) * B * r;
