@@ -152,6 +152,36 @@ def test_config2_full_parity(batch):
         gc.close()
 
 
+@pytest.mark.parametrize("workload,W,batch", [(1, 2, 1), (2, 32, 0)])
+@pytest.mark.parametrize("slow", ["compute", "copy"])
+def test_slot_reuse_gated_by_events_not_timing(workload, W, batch, slow):
+    """Slot reuse is ordered by HIP events, not by how fast either stream
+    runs.  Before every window a bounded spin kernel is queued on one of the
+    session's streams: on the compute stream the installs lag far behind the
+    copies, so a copy into a reused slot must wait for the release of the
+    chunk installed from it; on the copy stream the copies lag, so each
+    install must wait for its chunks' copies.  Either missing wait would
+    install the wrong bytes.  The image must be the oracle's."""
+    say(f"case: workload {workload}, W={W}, batch={batch}, slow {slow} stream")
+    wi = generate(get_config(workload))
+    case, n, _, _, res = _oracle(wi, W)
+    gc = GpuCase(wi, W=W, install_batch=batch)
+    try:
+        assert gc.probe(61)[0] == n
+        sess = gc.session
+        stream = sess.compute_stream if slow == "compute" else sess.copy_stream
+        torch.cuda.synchronize()
+        sess.bind(61, n, gc.dsts())
+        for first, cnt in sess.windows(n):
+            with torch.cuda.stream(stream):
+                torch.cuda._sleep(4_000_000)  # a spin kernel of a fixed cycle count
+            bsr.bsr_restore_window(gc.ctx, 61, first, cnt)
+        out = sess.commit(61)
+        _compare_success(gc, case, res, out)
+    finally:
+        gc.close()
+
+
 @pytest.mark.parametrize("mode,k", [("missing", 0), ("missing", 5), ("corrupt", 1), ("corrupt", 15),
                                     ("timeout", 7), ("transfer", 3), ("abort", 2)])
 def test_config1_failure_parity(mode, k):
