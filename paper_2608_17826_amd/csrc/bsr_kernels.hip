@@ -3,15 +3,16 @@
 // install : scatter staged chunks from the W-slot ring into every group's
 //           paged blocks (§3 "Install locally"; §4 windowed retrieve, whose
 //           per-window step moves the staged window into the engine's
-//           blocks).  One
-//           workgroup per piece of a (tensor, destination block) segment.
-//           Contiguous groups move 16-byte vectors ring -> pool, all loads of
-//           a piece issued before its destination is resolved; planar groups
-//           (records split into a values plane and a scales plane inside a
-//           block) stage the piece in LDS and write both planes with
-//           coalesced stores.  Every wave also folds the words it read into
-//           a (sum, xor) tag partial, and ballots the request's status words
-//           first, so no workgroup installs past a failure.
+//           blocks).  One workgroup per piece of a (tensor, destination
+//           block) segment.  A piece's 16-byte data loads and one
+//           lane-parallel metadata load (block id, tensor base, the
+//           request's status words) share one memory round trip; a ballot
+//           over the status lanes is the prefix check, so no workgroup
+//           installs past a failure.  Contiguous groups store the vectors
+//           straight to the pool; planar groups (records split into a values
+//           plane and a scales plane inside a block) stage the piece in LDS
+//           and write both planes with coalesced stores.  Every wave folds
+//           the words it read into a (sum, xor) tag partial.
 // verify  : reduce the partials of each (chunk, group) and compare with the
 //           tag recorded at store time; the first mismatching chunk, in
 //           chunk order, fails the request (q_g = 0 for its mismatching
