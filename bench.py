@@ -384,12 +384,26 @@ def recorded_traffic(workload_name, install_batch):
 
 
 def cpu_baseline(wi, W, target_s):
-    """The oracle, single-threaded, on the first windows of the same workload.
+    """The oracle, on one CPU, on the first windows of the same workload.
 
-    The sample restores whole windows (W chunks each) until about target_s
-    seconds of oracle work; destination pools are compacted to the blocks
-    the sample touches (block ids renumbered), which changes no arithmetic.
+    The calling thread is pinned to a single CPU while the oracle runs (its
+    numpy work is elementwise and runs on that thread).  The sample restores
+    whole windows (W chunks each) until about target_s seconds of oracle
+    work; destination pools are compacted to the blocks the sample touches
+    (block ids renumbered), which changes no arithmetic.
     """
+    prev = os.sched_getaffinity(0)
+    cpu = min(prev)
+    os.sched_setaffinity(0, {cpu})
+    try:
+        out = _cpu_baseline_pinned(wi, W, target_s)
+    finally:
+        os.sched_setaffinity(0, prev)
+    out["pinned_cpu"] = cpu
+    return out
+
+
+def _cpu_baseline_pinned(wi, W, target_s):
     import numpy as np
 
     import oracle
