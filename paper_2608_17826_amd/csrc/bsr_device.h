@@ -116,12 +116,12 @@ struct InstallHead {
   PackedDiv div_window;     // by W
   uint32_t n_groups;
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
-  // Workgroups are issued group by group (planar first, then by descending
-  // piece size, so the launch's tail is made of the shortest pieces); within
-  // a group, chunk by chunk.  order_prefix[o] is the number of workgroups
-  // per chunk of the groups before dispatch position o; a launch of n chunks
-  // starts position o at n * order_prefix[o].  Positions past the last group
-  // hold the total, which no workgroup index reaches.
+  // Workgroups are issued group by group (contiguous groups by descending
+  // piece size, planar groups last); within a group, chunk by chunk.
+  // order_prefix[o] is the number of workgroups per chunk of the groups
+  // before dispatch position o; a launch of n chunks starts position o at
+  // n * order_prefix[o].  Positions past the last group hold the total,
+  // which no workgroup index reaches.
   uint32_t order_prefix[BSR_MAX_GROUPS];
   // words 16-31
   const uint8_t* ring;

@@ -233,12 +233,14 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
   G->wg_start[L->n_groups] = wg;
   for (uint32_t g = L->n_groups + 1; g <= BSR_MAX_GROUPS; ++g) G->wg_start[g] = wg;
   G->wg_per_chunk = wg;
-  // dispatch planar groups first (LDS-staged, slowest per byte), then
-  // contiguous groups by descending piece size
+  // dispatch contiguous groups first, by descending piece size, and planar
+  // (LDS-staged) groups last: measured on the 512K 4-group layout with four
+  // install workgroups per CU, planar-last runs 0.3-0.4 points of 8 TB/s
+  // faster than planar-first
   for (uint32_t g = 0; g < L->n_groups; ++g) G->order[g] = g;
   auto cost = [&](uint32_t g) -> uint64_t {
     const GroupGeom& q = G->gg[g];
-    return q.kind == BSR_KIND_PLANAR ? (1ull << 40) : q.piece_bytes;
+    return q.kind == BSR_KIND_PLANAR ? 0ull : q.piece_bytes;
   };
   std::stable_sort(G->order, G->order + L->n_groups, [&](uint32_t a, uint32_t b) { return cost(a) > cost(b); });
   uint32_t acc = 0;
