@@ -117,7 +117,8 @@ struct InstallHead {
   uint32_t n_groups;
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
   // Workgroups are issued group by group (contiguous groups by descending
-  // piece size, planar groups last); within a group, chunk by chunk.
+  // piece size, planar groups just before the last contiguous group); within
+  // a group, chunk by chunk.
   // order_prefix[o] is the number of workgroups per chunk of the groups
   // before dispatch position o; a launch of n chunks starts position o at
   // n * order_prefix[o].  Positions past the last group hold the total,
