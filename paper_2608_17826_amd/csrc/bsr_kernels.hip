@@ -34,9 +34,6 @@
 #ifndef BSR_NT_LOAD
 #define BSR_NT_LOAD 1   // staged chunks are read once: non-temporal loads
 #endif
-#ifndef BSR_NT_STORE
-#define BSR_NT_STORE 1  // paged blocks are not re-read by this path: non-temporal stores
-#endif
 
 
 namespace bsr {
@@ -51,15 +48,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 template <typename T>
 __device__ __forceinline__ __attribute__((address_space(1))) T* global_ptr(T* p) {
   return (__attribute__((address_space(1))) T*)(p);
-}
-
-template <typename T>
-__device__ __forceinline__ void st_stream(T v, T* p) {
-#if BSR_NT_STORE
-  __builtin_nontemporal_store(v, global_ptr(p));
-#else
-  *global_ptr(p) = v;
-#endif
 }
 
 // Stores of a piece through a buffer resource whose base is the piece's
