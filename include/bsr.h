@@ -146,8 +146,8 @@ typedef struct bsr_config {
   uint32_t window_chunks;     /* W: staging slots, the restore-window size; 0 = legacy whole-plan mode
                                  (§4 "Restore-window configuration": each request's ring holds its whole
                                  plan, n_hit slots, none reused; peak staging n_hit * slot bytes, Eq. 2) */
-  uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W - W/8, at least 1, at most
-                                 BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
+  uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W up to W = 8, else W - W/8;
+                                 at most BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
                                  windows; a batch smaller than W keeps the copy engine busy across windows.
                                  BSR_E_ARG when one launch of this many chunks would exceed HIP's 2^32 - 1
                                  work-items (a layout of very many small tensors): lower it */

@@ -622,11 +622,14 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   // each request's ring holds its whole plan and no slot is reused.
   const uint32_t W = config->window_chunks;
   uint32_t b = config->install_batch;
-  // automatic: W - W/8 chunks per launch (at least 1): large launches, and
-  // W/8 chunk-copies of slack before a slot's next copy needs its install
+  // automatic: W - W/8 chunks per launch: large launches, and W/8
+  // chunk-copies of slack before a slot's next copy needs its install.  Up
+  // to W = 8 a launch takes the whole window (the slack would be one chunk,
+  // and measured at W = 8 the larger launch is faster: 52.7 against 52.1
+  // GB/s end to end, four alternating runs each)
   if (b == 0)
     b = W == 0 ? static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)
-               : std::max(1u, std::min(W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
+               : std::max(1u, std::min(W <= 8 ? W : W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
   if ((W && b > W) || b > BSR_MAX_INSTALL_BATCH)
     return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
   // admission (§3 "Install locally": one bounded restore at a time; §7: a
