@@ -12,7 +12,9 @@ import pytest
 
 import oracle
 import oracle.admission as adm
+import oracle.fnv as ofnv
 import oracle.keys as okeys
+import oracle.layout as olayout
 import oracle.restore as orest
 import oracle.store as ostore
 import oracle.tag as otag
@@ -41,6 +43,10 @@ def _pins():
         ("tag word loop", t_fnv.test_tag_matches_word_loop),
         ("admission exact fit", t_adm.test_exact_fit_and_release),
         ("admission lock", t_adm.test_budget_zero_is_a_lock),
+        ("FNV-1a published vectors", lambda: [t_fnv.test_fnv1a64_published_vectors(e, d) for e, d in t_fnv._vectors()]),
+        ("one group missing shortens the prefix", t_probe.test_one_group_missing_before_probe_shortens_prefix),
+        ("abort after a window", t_fail.test_abort_after_window),
+        ("slot offsets aligned", t_rest.test_slot_offsets_align_every_group_to_256),
     ]
     for s in range(3):
         pins.append((f"random layout brute force {s}", lambda s=s: t_rest.test_random_layout_bruteforce(s)))
@@ -174,6 +180,101 @@ def _admission_end_releases_nothing(mp):
     mp.setattr(adm, "replay", replay)
 
 
+def _fnv1_instead_of_fnv1a(mp):
+    def fnv1(data, h=ofnv.FNV64_OFFSET_BASIS):
+        for octet in data:      # multiply before the XOR: FNV-1, not FNV-1a
+            h = (h * ofnv.FNV64_PRIME) & ofnv.MASK64
+            h ^= octet
+        return h
+    for mod in (ofnv, okeys, t_fnv):
+        mp.setattr(mod, "fnv1a64", fnv1)
+
+
+def _fnv_prime_off_by_two(mp):
+    def f(data, h=ofnv.FNV64_OFFSET_BASIS):
+        for octet in data:
+            h ^= octet
+            h = (h * (ofnv.FNV64_PRIME + 2)) & ofnv.MASK64
+        return h
+    for mod in (ofnv, okeys, t_fnv):
+        mp.setattr(mod, "fnv1a64", f)
+
+
+def _slot_groups_not_aligned(mp):
+    mp.setattr(olayout, "align_up", lambda x, a=olayout.ALIGN: x)
+
+
+def _commit_ignores_failed_window(mp):
+    orig = orest.windowed_restore
+
+    def restore(layout, store, keys, n_hit, W, block_tables, pools, valid, **kw):
+        res = orig(layout, store, keys, n_hit, W, block_tables, pools, valid, **kw)
+        if res.fail_reason != orest.FAIL_NONE and all(res.q):   # Q computed from q_g alone
+            orest.set_request_valid(layout, n_hit, block_tables, valid, 1)
+            res.exposed_tokens, res.fallback = n_hit * layout.chunk_tokens, 0
+        return res
+    mp.setattr(orest, "windowed_restore", restore)
+    mp.setattr(oracle, "windowed_restore", restore)
+
+
+def _invalidate_failed_groups_only(mp):
+    orig = orest.windowed_restore
+
+    def restore(layout, store, keys, n_hit, W, block_tables, pools, valid, **kw):
+        res = orig(layout, store, keys, n_hit, W, block_tables, pools, valid, **kw)
+        if res.fallback:        # groups that did not fail keep their blocks valid
+            for g, gr in enumerate(layout.groups):
+                if res.q[g]:
+                    for k in range(orest.request_blocks(n_hit, layout.chunk_tokens, gr.block_tokens)):
+                        valid[g][int(block_tables[g][k])] = 1
+        return res
+    mp.setattr(orest, "windowed_restore", restore)
+    mp.setattr(oracle, "windowed_restore", restore)
+
+
+def _probe_any_group(mp):
+    def probe(store, tokens, chunk_tokens, salt, force_local=False):
+        keys = okeys.chain_keys(tokens, chunk_tokens, salt)
+        bitmap = np.zeros(len(keys), dtype=np.uint8)
+        if force_local:
+            return 0, bitmap, keys
+        for i, h in enumerate(keys):     # any group's entry instead of every group's
+            bitmap[i] = any(store.has(h, g) for g in range(store.n_groups))
+        n = 0
+        while n < len(keys) and bitmap[n]:
+            n += 1
+        return n, bitmap, keys
+    mp.setattr(orest, "probe", probe)
+    mp.setattr(oracle, "probe", probe)
+
+
+def _install_mapping(mp, in_block_offset=True, tensor_major=True):
+    def install(layout, i, slot, block_tables, pools):
+        C = layout.chunk_tokens
+        offs = layout.group_offsets()
+        for g, gr in enumerate(layout.groups):
+            flat = slot[offs[g]:offs[g] + layout.payload_bytes(g)]
+            region = (flat.reshape(gr.n_tensors, C, gr.record_bytes) if tensor_major
+                      else flat.reshape(C, gr.n_tensors, gr.record_bytes).transpose(1, 0, 2))
+            for t in range(gr.n_tensors):
+                q = 0
+                while q < C:
+                    k, o = divmod(i * C + q, gr.block_tokens)
+                    m = min(gr.block_tokens - o, C - q)
+                    orest._place(layout, g, pools[g][t, int(block_tables[g][k])],
+                                 o if in_block_offset else 0, region[t, q:q + m])
+                    q += m
+    mp.setattr(orest, "install_chunk", install)
+
+
+def _in_block_offset_dropped(mp):
+    _install_mapping(mp, in_block_offset=False)
+
+
+def _tensor_and_token_axes_swapped(mp):
+    _install_mapping(mp, tensor_major=False)
+
+
 MUTANTS = {
     "planar plane offset": _planar_plane_offset,
     "block index ignores the table": _block_index_ignores_table,
@@ -184,6 +285,14 @@ MUTANTS = {
     "tag sum and xor swapped": _tag_sum_and_xor_swapped,
     "admission budget strict": _admission_strict_budget,
     "admission end releases nothing": _admission_end_releases_nothing,
+    "FNV-1 instead of FNV-1a": _fnv1_instead_of_fnv1a,
+    "FNV prime off by two": _fnv_prime_off_by_two,
+    "slot groups not 256-aligned": _slot_groups_not_aligned,
+    "commit ignores a failed window": _commit_ignores_failed_window,
+    "invalidate the failed groups only": _invalidate_failed_groups_only,
+    "probe accepts any group": _probe_any_group,
+    "in-block token offset dropped": _in_block_offset_dropped,
+    "tensor and token axes swapped": _tensor_and_token_axes_swapped,
 }
 
 

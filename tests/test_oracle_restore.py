@@ -206,3 +206,15 @@ def test_expected_block_matches_full_restore():
                 e = oracle.expected_block(case.layout, case.store, case.keys, n, wi.block_tables[g],
                                           g, t, b, wi.sentinel_pool(g)[t, b])
                 np.testing.assert_array_equal(e, case.pools[g][t, b])
+
+
+def test_slot_offsets_align_every_group_to_256():
+    """Slot layout reading: each group's entry starts 256-byte aligned inside a
+    staged chunk; worked by hand for payloads that are not 256 multiples."""
+    from oracle.layout import OracleGroup, OracleLayout
+    L = OracleLayout(8, (OracleGroup(4, 3, 12, "contig", 0), OracleGroup(8, 1, 20, "planar", 16)))
+    # payloads: 3 tensors x 8 tokens x 12 B = 288 B, then 1 x 8 x 20 = 160 B
+    assert [L.payload_bytes(0), L.payload_bytes(1)] == [288, 160]
+    assert L.group_offsets() == [0, 512]
+    assert L.slot_bytes == 768
+    assert L.chunk_payload_bytes == 448
