@@ -114,7 +114,7 @@ def test_random_layout_parity(seed):
             gc.close()
 
 
-@pytest.mark.parametrize("seed", range(10, 20))
+@pytest.mark.parametrize("seed", range(10, 110))
 def test_random_layout_batch_and_flags_parity(seed):
     """Random layouts with a seeded window, install batch size and block-table
     check (host readback or device check), against the oracle image."""
