@@ -224,7 +224,7 @@ def test_config1_failure_parity(mode, k):
         gc.close()
 
 
-@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("seed", range(50))
 def test_random_layout_failure_parity(seed):
     """Random layouts x a seeded fault (missing / corrupt entry in a random
     group, timeout, transfer error, abort) at a seeded chunk."""
