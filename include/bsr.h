@@ -382,7 +382,8 @@ int bsr_probe(bsr_ctx* ctx, uint64_t request_id, uint64_t salt, const int32_t* t
  * than B alone is BSR_E_STAGING).  Concurrently bound requests need their
  * own staging rings and status blocks (overlap -> BSR_E_ARG) and must not
  * share destination blocks; they may share streams.  n_hit_chunks <= the
- * probed n.
+ * probed n, and n_hit_chunks * chunk_tokens plus twice the largest
+ * block_tokens must stay below 2^32 (else BSR_E_ARG).
  * dst: n_groups destinations (block tables are copied to the host once and
  * checked: every id < pool_blocks, no id repeated -> else BSR_E_ARG; with
  * BSR_FLAG_TRUSTED_TABLES they are checked on the device instead, see the

@@ -272,7 +272,7 @@ struct SegMeta {
 };
 
 __device__ __forceinline__ const uint32_t* meta_addr(const bsr_dev_status* status, const int32_t* block_table,
-                                                     uint8_t* const* tensor_bases, uint64_t k, uint32_t t,
+                                                     uint8_t* const* tensor_bases, uint32_t k, uint32_t t,
                                                      uint32_t lane) {
   const uint32_t* st = reinterpret_cast<const uint32_t*>(status);
   const uint32_t* a = st;  // lane 3 and every lane past the q words: the fail word
@@ -317,6 +317,15 @@ __device__ __forceinline__ T load_args(const T* src) {
   return w.s;
 }
 
+// acc + (a >= b) for wave-uniform a, b: a scalar compare and an add of its
+// carry.  (Written as C, the comparison becomes a lane mask that is turned
+// back into an integer through a vector register, several instructions and
+// a vector-to-scalar transfer per comparison.)
+__device__ __forceinline__ uint32_t add_if_ge(uint32_t acc, uint32_t a, uint32_t b) {
+  asm("s_cmp_ge_u32 %1, %2\n\ts_addc_u32 %0, %0, 0" : "+s"(acc) : "s"(a), "s"(b) : "scc");
+  return acc;
+}
+
 __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams p) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
 
@@ -325,17 +334,18 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   const InstallHead H = load_args(&p.h);
   // work index -> dispatch position (the group), then (chunk, piece within
   // the chunk's group range)
-  const uint32_t bid = blockIdx.x;
-  uint32_t oi = 0, base = 0;
+  const uint32_t bid = xcd_work_index(blockIdx.x, H.xcd_full);
+  // Every wave of the workgroup runs this decode on the scalar unit, which
+  // the CU's waves share: it is kept to a few dozen scalar instructions
+  // (a 256-instruction scalar prologue costs a plain copy of this shape about
+  // 3 points of HBM bandwidth, 128 instructions 0.3).  The dispatch position
+  // is the count of group starts at or below bid (the starts increase with
+  // the position).
+  uint32_t oi = 0;
 #pragma unroll
-  for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) {
-    const uint32_t start = H.n_chunks * H.order_prefix[q];
-    const bool in = bid >= start;  // the prefix is increasing: the last start at or below bid wins
-    oi = in ? q : oi;
-    base = in ? start : base;
-  }
+  for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) oi = add_if_ge(oi, bid, H.start[q]);
   const InstallGroup G = load_args(&p.g[oi]);
-  uint32_t rem = bid - base;
+  uint32_t rem = bid - H.n_chunks * G.prefix;
   const uint32_t c = packed_div(G.div_per_chunk.m, G.div_per_chunk.s, rem);
   rem -= c * G.per_chunk;
   const uint32_t wg = c * H.wg_per_chunk + G.wg_start + rem;  // chunk-major slot of the tag partials
@@ -346,23 +356,26 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   const uint32_t j = r1 - t * G.segs_per_chunk;
 
   const uint32_t chunk = H.first_chunk + c;
-  const uint32_t slot = chunk - packed_div(H.div_window.m, H.div_window.s, chunk) * H.window;
-  const uint64_t C = H.chunk_tokens, B = G.block_tokens;
-  const uint32_t tok0_32 = chunk * H.chunk_tokens;  // the bound prefix has < 2^32 tokens
-  const uint64_t tok0 = tok0_32;
-  const uint64_t k = packed_div(G.div_block.m, G.div_block.s, tok0_32) + j;  // request block index
-  const uint64_t blo = k * B;
-  const uint64_t lo = tok0 > blo ? tok0 : blo;
-  const uint64_t hi = (tok0 + C) < (blo + B) ? (tok0 + C) : (blo + B);
+  const uint32_t slot0 = H.first_slot + c;  // c < n_chunks <= W
+  const uint32_t slot = slot0 >= H.window ? slot0 - H.window : slot0;
+  // Token positions in 32 bits: the bound prefix plus two blocks stays
+  // below 2^32 tokens (checked when the request is bound).
+  const uint32_t C = H.chunk_tokens, B = G.block_tokens;
+  const uint32_t tok0 = chunk * C;
+  const uint32_t k = packed_div(G.div_block.m, G.div_block.s, tok0) + j;  // request block index
+  const uint32_t blo = k * B;
+  const uint32_t lo = tok0 > blo ? tok0 : blo;
+  const uint32_t hi = (tok0 + C) < (blo + B) ? (tok0 + C) : (blo + B);
 
   uint32_t s = 0, x = 0;
   if (lo < hi && k < G.n_blocks) {
     const uint32_t r = G.record_bytes;
-    const uint32_t m = static_cast<uint32_t>(hi - lo);
-    const uint32_t q0 = static_cast<uint32_t>(lo - tok0);
-    const uint32_t o0 = static_cast<uint32_t>(lo - blo);
-    const uint8_t* src = H.ring + static_cast<uint64_t>(slot) * H.slot_bytes + G.staged_off +
-                         (static_cast<uint64_t>(t) * C + q0) * r;
+    const uint32_t m = hi - lo;
+    const uint32_t q0 = lo - tok0;
+    const uint32_t o0 = lo - blo;
+    // offsets inside a slot and inside a block fit 32 bits (slot < 4 GiB,
+    // block < 2 GiB)
+    const uint8_t* src = H.ring + static_cast<uint64_t>(slot) * H.slot_bytes + (G.staged_off + (t * C + q0) * r);
     if (G.kind == BSR_KIND_CONTIG) {
       const uint32_t seg = m * r;
       const uint32_t off = piece * G.piece;
@@ -390,7 +403,7 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       LoadBurst<U>::run(v, mw, at, meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
       const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
       if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && len) {
-        uint8_t* dp = md.tensor_base + static_cast<uint64_t>(md.block) * B * r + static_cast<uint64_t>(o0) * r + off;
+        uint8_t* dp = md.tensor_base + static_cast<uint64_t>(md.block) * G.block_bytes + (o0 * r + off);
         if (one_pass && (reinterpret_cast<uintptr_t>(dp) & 15u) == 0) {
           const __amdgpu_buffer_rsrc_t rs = piece_rsrc(dp, len);
 #pragma unroll
@@ -409,7 +422,7 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       const uint32_t sp = G.split_bytes;
       const uint32_t u0 = piece * G.piece;
       const uint32_t mu = u0 < m ? ((m - u0) < G.piece ? (m - u0) : G.piece) : 0;
-      const uint8_t* psrc = src + static_cast<uint64_t>(u0) * r;
+      const uint8_t* psrc = src + u0 * r;
       const uint32_t bytes = mu * r;
       const uint32_t nvec = bytes >> 4;
       const bool src_ok =
@@ -429,9 +442,9 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
       LoadBurst<kPlanarVecs>::run(v, mw, at, meta_addr(H.status, G.block_table, G.tensor_bases, k, t, lane));
       const SegMeta md = broadcast_meta(mw, lane, H.n_groups);
       if (!md.past_prefix && md.block >= 0 && static_cast<uint32_t>(md.block) < G.pool_blocks && mu) {
-        uint8_t* blk = md.tensor_base + static_cast<uint64_t>(md.block) * B * r;
-        uint8_t* dst1 = blk + static_cast<uint64_t>(o0 + u0) * sp;
-        uint8_t* dst2 = blk + B * sp + static_cast<uint64_t>(o0 + u0) * (r - sp);
+        uint8_t* blk = md.tensor_base + static_cast<uint64_t>(md.block) * G.block_bytes;
+        uint8_t* dst1 = blk + (o0 + u0) * sp;
+        uint8_t* dst2 = blk + (B * sp + (o0 + u0) * (r - sp));
         if (src_ok && ((reinterpret_cast<uintptr_t>(dst1) & 15u) | (reinterpret_cast<uintptr_t>(dst2) & 3u)) == 0)
           planar_from_regs(v, nvec, dst1, dst2, mu, r, sp, G.div_p1, G.div_p2, lds, tid, s, x);
         else
@@ -584,6 +597,8 @@ __global__ __launch_bounds__(256) void k_finish(const FinishParams p) {
 
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s, hipEvent_t start,
                           hipEvent_t stop) {
+  // the XCD remap is a permutation of the grid only for whole spans inside it
+  if (p.h.xcd_full != xcd_remap_bound(n_workgroups)) return hipErrorInvalidValue;
   if (start && stop) {
     // the events are stamped by the kernel's own dispatch (no marker packets)
     hipExtLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.h.lds_bytes, s, start, stop, 0, p);

@@ -468,9 +468,16 @@ int flush_batch(bsr_ctx* c, Session& s) {
   if ((rc = hip_check(hipEventRecord(full, s.copy), "hipEventRecord(full)"))) return rc;
   if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
 
+  // the kernel takes chunk first_chunk + c to slot first_slot + c, less W
+  // once: a launch holds consecutive chunks, at most W of them
+  if (chunks.size() > s.window || chunks.back() - chunks.front() + 1 != chunks.size())
+    return fail_with(BSR_E_STATE, "install batch of %zu chunks is not a run of at most W = %u", chunks.size(), s.window);
   InstallParams ip = s.ip;
   ip.h.n_chunks = static_cast<uint32_t>(chunks.size());
   ip.h.first_chunk = chunks.front();
+  ip.h.first_slot = chunks.front() % s.window;
+  for (uint32_t o = 0; o < BSR_MAX_GROUPS; ++o) ip.h.start[o] = ip.h.n_chunks * c->geo.order_prefix[o];
+  ip.h.xcd_full = bsr::xcd_remap_bound(ip.h.n_chunks * ip.h.wg_per_chunk);
   hipEvent_t t0 = nullptr, t1 = nullptr;
   if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
@@ -996,8 +1003,14 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   // Arguments and block tables first, without the context lock: the
   // readback waits for the caller's compute stream, and other requests'
   // calls must not wait for it.  The geometry read here never changes.
-  if (static_cast<uint64_t>(n_hit) * c->geo.L.chunk_tokens >= (1ull << 32))
-    return fail_with(BSR_E_ARG, "a restored prefix must be shorter than 2^32 tokens");
+  // the install kernel's token arithmetic is 32-bit: the prefix plus two of
+  // the largest blocks must stay below 2^32 tokens
+  {
+    uint64_t max_b = 0;
+    for (uint32_t g = 0; g < c->geo.L.n_groups; ++g) max_b = std::max<uint64_t>(max_b, c->geo.L.groups[g].block_tokens);
+    if (static_cast<uint64_t>(n_hit) * c->geo.L.chunk_tokens + 2 * max_b >= (1ull << 32))
+      return fail_with(BSR_E_ARG, "a restored prefix must be shorter than 2^32 tokens less two blocks");
+  }
   if (!dst || !staging || !status) return fail_with(BSR_E_ARG, "dst, staging or status is NULL");
   if (!copy_stream || !compute_stream || copy_stream == compute_stream)
     return fail_with(BSR_E_ARG, "copy and compute streams must be distinct non-null streams");
@@ -1020,11 +1033,9 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   ip.h.ring = static_cast<const uint8_t*>(staging);
   ip.h.slot_bytes = c->geo.slot_bytes;
   ip.h.window = window;
-  ip.h.div_window = bsr::pack_fastdiv(bsr::make_fastdiv(window));
   ip.h.chunk_tokens = C;
   ip.h.n_groups = G;
   ip.h.wg_per_chunk = c->geo.wg_per_chunk;
-  for (uint32_t o = 0; o < BSR_MAX_GROUPS; ++o) ip.h.order_prefix[o] = c->geo.order_prefix[o];
   ip.h.lds_bytes = c->geo.lds_bytes;
   ip.h.status = status;
   uint32_t total = 0;
@@ -1076,6 +1087,8 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     ig.block_table = d.block_table;
     ig.tensor_bases = reinterpret_cast<uint8_t* const*>(d.tensor_bases);
     ig.group = g;
+    ig.prefix = c->geo.order_prefix[pos];
+    ig.block_bytes = q.block_tokens * q.record_bytes;
     if (q.kind == BSR_KIND_PLANAR) {
       ig.div_p1 = bsr::pack_fastdiv(bsr::make_fastdiv(std::max(1u, q.split_bytes / 16)));
       ig.div_p2 = bsr::pack_fastdiv(bsr::make_fastdiv((q.record_bytes - q.split_bytes) / 4));
