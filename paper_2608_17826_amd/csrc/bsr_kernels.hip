@@ -4,15 +4,16 @@
 //           paged blocks (§3 "Install locally"; §4 windowed retrieve, whose
 //           per-window step moves the staged window into the engine's
 //           blocks).  One workgroup per piece of a (tensor, destination
-//           block) segment.  A piece's 16-byte data loads and one
-//           lane-parallel metadata load (block id, tensor base, the
-//           request's status words) share one memory round trip; a ballot
-//           over the status lanes is the prefix check, so no workgroup
-//           installs past a failure.  Contiguous groups store the vectors
-//           straight to the pool; planar groups (records split into a values
-//           plane and a scales plane inside a block) stage the piece in LDS
-//           and write both planes with coalesced stores.  Every wave folds
-//           the words it read into a (sum, xor) tag partial.
+//           block) segment; consecutive pieces are issued in runs to one
+//           XCD, so a block's pieces share an L2.  A piece's 16-byte data
+//           loads and one lane-parallel metadata load (block id, tensor
+//           base, the request's status words) share one memory round trip;
+//           a ballot over the status lanes is the prefix check, so no
+//           workgroup installs past a failure.  Contiguous groups store the
+//           vectors straight to the pool; planar groups (records split into
+//           a values plane and a scales plane inside a block) stage the
+//           piece in LDS and write both planes with coalesced stores.  Every
+//           wave folds the words it read into a (sum, xor) tag partial.
 // verify  : reduce the partials of each (chunk, group) and compare with the
 //           tag recorded at store time; the first mismatching chunk, in
 //           chunk order, fails the request (q_g = 0 for its mismatching
@@ -336,11 +337,11 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   // the chunk's group range)
   const uint32_t bid = xcd_work_index(blockIdx.x, H.xcd_full);
   // Every wave of the workgroup runs this decode on the scalar unit, which
-  // the CU's waves share: it is kept to a few dozen scalar instructions
-  // (a 256-instruction scalar prologue costs a plain copy of this shape about
-  // 3 points of HBM bandwidth, 128 instructions 0.3).  The dispatch position
-  // is the count of group starts at or below bid (the starts increase with
-  // the position).
+  // the CU's waves share, so it is kept short: about 120 scalar instructions
+  // before the first data load (256 extra scalar instructions per wave cost
+  // a plain copy of this shape about 3 points of HBM bandwidth, 128 about
+  // 0.3).  The dispatch position is the count of group starts at or below
+  // bid (the starts increase with the position).
   uint32_t oi = 0;
 #pragma unroll
   for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) oi = add_if_ge(oi, bid, H.start[q]);

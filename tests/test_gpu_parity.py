@@ -462,3 +462,26 @@ def test_empty_prefix_and_new_salt(W):
             np.testing.assert_array_equal(gc.pool_host(g), wi.sentinel_pool(g))
     finally:
         gc.close()
+
+
+def test_bind_refuses_prefixes_past_the_32_bit_token_range():
+    """The install works on 32-bit token positions: bind refuses a prefix
+    whose tokens plus two of the largest blocks reach 2^32, and lets the
+    largest prefix below that through to its next check (here the missing
+    destinations, so nothing is bound)."""
+    wi = generate(get_config(1))             # 64-token chunks, 16-token blocks
+    gc = GpuCase(wi, W=2)
+    try:
+        C, B = 64, 16
+        limit = (2**32 - 2 * B) // C         # largest n with n*C + 2B < 2^32 (n*C + 2B = 2^32 - 64 + 32)
+        assert limit * C + 2 * B < 2**32 <= (limit + 1) * C + 2 * B
+        say(f"case: bind bound at n_hit={limit + 1} (refused) and {limit} (passes the bound)")
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_request_bind(gc.ctx, 91, limit + 1, [], 0, 0, 0, 0, 0)
+        assert e.value.code == bsr.BSR_E_ARG and "2^32" in str(e.value)
+        with pytest.raises(bsr.BsrError) as e:
+            bsr.bsr_request_bind(gc.ctx, 91, limit, [], 0, 0, 0, 0, 0)
+        assert e.value.code == bsr.BSR_E_ARG and "2^32" not in str(e.value) and "NULL" in str(e.value)
+        assert bsr.bsr_admission_get(gc.ctx)["n_bound"] == 0
+    finally:
+        gc.close()
