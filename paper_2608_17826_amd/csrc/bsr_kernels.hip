@@ -467,8 +467,15 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
 // One workgroup per (chunk, group) of the launch reduces that entry's wave
 // partials and compares with the stored tag; the last workgroup to finish
 // applies the first mismatching chunk, in chunk order, to the status words
-// and leaves the shared words zeroed for the next launch.
-__global__ __launch_bounds__(256) void k_verify(const VerifyParams p) {
+// and leaves the shared words zeroed for the next launch.  Both halves are
+// latency-bound, so each keeps its memory accesses in flight together: a
+// thread loads up to kVerifyUnroll partials before adding any, and the last
+// workgroup takes every chunk's mismatch word in one exchange per lane.
+constexpr uint32_t kVerifyThreads = 256;
+constexpr uint32_t kVerifyUnroll = 8;
+static_assert(BSR_MAX_INSTALL_BATCH <= 64, "one lane of the first wave per chunk of a launch");
+
+__global__ __launch_bounds__(kVerifyThreads) void k_verify(const VerifyParams p) {
   __shared__ uint32_t red_s[4], red_x[4];
   __shared__ uint32_t is_last;
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -479,10 +486,18 @@ __global__ __launch_bounds__(256) void k_verify(const VerifyParams p) {
   if (live) {
     const uint32_t lo = (c * p.wg_per_chunk + p.wg_start[g]) * kInstallWaves;
     const uint32_t hi = (c * p.wg_per_chunk + p.wg_start[g + 1]) * kInstallWaves;
-    for (uint32_t i = lo + tid; i < hi; i += 256) {
-      const TagPair tp = p.partials[i];
-      s += tp.sum;
-      x ^= tp.x;
+    for (uint32_t i0 = lo + tid; i0 < hi; i0 += kVerifyThreads * kVerifyUnroll) {
+      TagPair tp[kVerifyUnroll];
+#pragma unroll
+      for (uint32_t u = 0; u < kVerifyUnroll; ++u) {
+        const uint32_t i = i0 + u * kVerifyThreads;
+        tp[u] = i < hi ? p.partials[i] : TagPair{0u, 0u};
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kVerifyUnroll; ++u) {
+        s += tp[u].sum;
+        x ^= tp[u].x;
+      }
     }
   }
   s = wave_sum(s);
@@ -503,20 +518,20 @@ __global__ __launch_bounds__(256) void k_verify(const VerifyParams p) {
     is_last = atomicAdd(&p.aux->arrivals, 1u) == gridDim.x - 1;
   }
   __syncthreads();
-  if (is_last && tid == 0) {
+  if (is_last && wave == 0) {
     __threadfence();
-    bool applied = !live;
-    for (uint32_t cc = 0; cc < p.n_chunks; ++cc) {
-      const uint32_t m = atomicExch(&p.aux->bad[cc], 0u);
-      if (m && !applied) {
-        p.status->fail = BSR_FAIL_CORRUPT;
-        p.status->first_failed_chunk = p.first_chunk + cc;
-        for (uint32_t gg = 0; gg < p.n_groups; ++gg)
-          if ((m >> gg) & 1u) p.status->q[gg] = 0;
-        applied = true;
-      }
+    // lane cc takes chunk cc's mismatch mask and leaves the word zeroed
+    const uint32_t m = lane < p.n_chunks ? atomicExch(&p.aux->bad[lane], 0u) : 0u;
+    const uint64_t any = __ballot(m != 0u);
+    // the first mismatching chunk in chunk order fails the request, unless a
+    // failure was recorded before this launch
+    if (live && any != 0ull && lane == static_cast<uint32_t>(__builtin_ctzll(any))) {
+      p.status->fail = BSR_FAIL_CORRUPT;
+      p.status->first_failed_chunk = p.first_chunk + lane;
+      for (uint32_t gg = 0; gg < p.n_groups; ++gg)
+        if ((m >> gg) & 1u) p.status->q[gg] = 0;
     }
-    atomicExch(&p.aux->arrivals, 0u);
+    if (lane == 0) atomicExch(&p.aux->arrivals, 0u);
   }
 }
 
@@ -610,7 +625,7 @@ hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStre
 }
 
 hipError_t launch_verify(const VerifyParams& p, hipStream_t s) {
-  hipLaunchKernelGGL(k_verify, dim3(p.n_chunks * p.n_groups), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(k_verify, dim3(p.n_chunks * p.n_groups), dim3(kVerifyThreads), 0, s, p);
   return hipGetLastError();
 }
 
