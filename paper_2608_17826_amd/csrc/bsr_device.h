@@ -46,29 +46,38 @@ constexpr uint32_t kLdsCapBytes = BSR_PLANAR_PIECE_BYTES;
 #define BSR_XCD_RUN 36
 #endif
 // Work order across the XCDs.  The dispatcher hands workgroup b of a launch
-// to XCD b mod 8, so consecutive work items (the pieces of one destination
-// block) would run on eight XCDs behind eight L2s.  The install remaps b so
-// that each XCD takes runs of kXcdRun consecutive work items instead: the
+// to XCD b mod X (X = 2^xcd_log2 XCDs in the device's partition: 8 on a
+// whole MI355X), so consecutive work items (the pieces of one destination
+// block) would run on X XCDs behind X L2s.  The install remaps b so that
+// each XCD takes runs of kXcdRun consecutive work items instead: the
 // pieces of a block then reach memory from one XCD.  Measured as a plain
-// copy of the install's shape into random 73.7 KB blocks: 69.5% of 8 TB/s
-// round robin, 77.3% with runs of 9 (one block), 78.2% with 18, 77.9% with
-// 36; into blocks in identity order 82% either way.  Any XCD count gives a
-// permutation; only the speed assumes eight.
-constexpr uint32_t kXcds = 8;
+// copy of the install's shape into random 73.7 KB blocks on eight XCDs:
+// 69.5% of 8 TB/s round robin, 77.3% with runs of 9 (one block), 78.2% with
+// 18, 77.9% with 36; into blocks in identity order 82% either way.  The
+// remap is a permutation for any X; with one XCD it is the identity.
 constexpr uint32_t kXcdRun = BSR_XCD_RUN;
-constexpr uint32_t kXcdSpan = kXcds * kXcdRun;
 static_assert(kXcdRun >= 1, "runs of at least one work item (1: round robin)");
+// log2 of the XCD count the host reads from the device (a power of two;
+// anything else is rounded down).
+inline uint32_t xcd_log2_of(int n_xcds) {
+  uint32_t l = 0;
+  while (n_xcds > 1 && (2 << l) <= n_xcds) ++l;
+  return l;
+}
 // Work items below the returned bound are remapped (whole spans of
-// kXcdSpan); the ragged rest keeps its order.
-inline uint32_t xcd_remap_bound(uint32_t grid) { return kXcdRun > 1 ? grid / kXcdSpan * kXcdSpan : 0; }
+// X * kXcdRun); the ragged rest keeps its order.
+inline uint32_t xcd_remap_bound(uint32_t grid, uint32_t xcd_log2) {
+  const uint32_t span = kXcdRun << xcd_log2;
+  return kXcdRun > 1 && xcd_log2 > 0 ? grid / span * span : 0;
+}
 
 #if defined(__HIP__)
 // Work item of hardware workgroup b (a permutation of [0, grid) whenever
-// full = xcd_remap_bound(grid)).
-__device__ __forceinline__ uint32_t xcd_work_index(uint32_t b, uint32_t full) {
+// full = xcd_remap_bound(grid, xcd_log2)).
+__device__ __forceinline__ uint32_t xcd_work_index(uint32_t b, uint32_t full, uint32_t xcd_log2) {
   if (b >= full) return b;
-  const uint32_t xcd = b % kXcds, local = b / kXcds;
-  return local / kXcdRun * kXcdSpan + xcd * kXcdRun + local % kXcdRun;
+  const uint32_t xcd = b & ((1u << xcd_log2) - 1u), local = b >> xcd_log2;
+  return ((local / kXcdRun * kXcdRun) << xcd_log2) + xcd * kXcdRun + local % kXcdRun;
 }
 #endif
 
@@ -144,7 +153,7 @@ struct InstallHead {
   uint32_t chunk_tokens;
   uint32_t window;          // W (slots in the ring)
   uint32_t first_slot;      // first_chunk mod W
-  uint32_t pad0;
+  uint32_t xcd_log2;        // log2 of the XCDs the dispatcher deals workgroups to
   uint32_t n_groups;
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
   // Workgroups are issued group by group (contiguous groups by descending

@@ -335,7 +335,7 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   const InstallHead H = load_args(&p.h);
   // work index -> dispatch position (the group), then (chunk, piece within
   // the chunk's group range)
-  const uint32_t bid = xcd_work_index(blockIdx.x, H.xcd_full);
+  const uint32_t bid = xcd_work_index(blockIdx.x, H.xcd_full, H.xcd_log2);
   // Every wave of the workgroup runs this decode on the scalar unit, which
   // the CU's waves share, so it is kept short: about 120 scalar instructions
   // before the first data load (256 extra scalar instructions per wave cost
@@ -614,7 +614,7 @@ __global__ __launch_bounds__(256) void k_finish(const FinishParams p) {
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s, hipEvent_t start,
                           hipEvent_t stop) {
   // the XCD remap is a permutation of the grid only for whole spans inside it
-  if (p.h.xcd_full != xcd_remap_bound(n_workgroups)) return hipErrorInvalidValue;
+  if (p.h.xcd_log2 > 5 || p.h.xcd_full != xcd_remap_bound(n_workgroups, p.h.xcd_log2)) return hipErrorInvalidValue;
   if (start && stop) {
     // the events are stamped by the kernel's own dispatch (no marker packets)
     hipExtLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.h.lds_bytes, s, start, stop, 0, p);

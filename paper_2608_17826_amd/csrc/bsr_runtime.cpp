@@ -397,6 +397,7 @@ struct bsr_ctx {
   Inject inject;          // armed for the next bind
   uint64_t partials_bytes = 0;  // per session slot
   uint64_t aux_bytes = 0;       // device bytes per session slot
+  uint32_t xcd_log2 = 3;        // log2 of the XCDs of the device's partition
   std::vector<hipEvent_t> timing_pool;
 };
 
@@ -477,7 +478,7 @@ int flush_batch(bsr_ctx* c, Session& s) {
   ip.h.first_chunk = chunks.front();
   ip.h.first_slot = chunks.front() % s.window;
   for (uint32_t o = 0; o < BSR_MAX_GROUPS; ++o) ip.h.start[o] = ip.h.n_chunks * c->geo.order_prefix[o];
-  ip.h.xcd_full = bsr::xcd_remap_bound(ip.h.n_chunks * ip.h.wg_per_chunk);
+  ip.h.xcd_full = bsr::xcd_remap_bound(ip.h.n_chunks * ip.h.wg_per_chunk, ip.h.xcd_log2);
   hipEvent_t t0 = nullptr, t1 = nullptr;
   if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
@@ -709,6 +710,13 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
                        lds_per_block);
     }
     c->geo.lds_bytes = std::max(c->geo.lds_bytes, share);
+    // XCDs the dispatcher deals the install's workgroups to (eight on a
+    // whole MI355X; fewer in a partitioned one); eight if the runtime cannot say
+    int n_xcds = 0;
+    if (hipDeviceGetAttribute(&n_xcds, hipDeviceAttributeNumberOfXccs, c->device) == hipSuccess && n_xcds >= 1)
+      c->xcd_log2 = bsr::xcd_log2_of(n_xcds);
+    else
+      (void)hipGetLastError();
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
     c->aux_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
     // event ring: the copy of chunk i waits for the release of chunk i - W,
@@ -1037,6 +1045,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   ip.h.n_groups = G;
   ip.h.wg_per_chunk = c->geo.wg_per_chunk;
   ip.h.lds_bytes = c->geo.lds_bytes;
+  ip.h.xcd_log2 = c->xcd_log2;
   ip.h.status = status;
   uint32_t total = 0;
   std::vector<int32_t> bt;
