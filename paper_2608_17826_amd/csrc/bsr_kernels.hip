@@ -98,12 +98,34 @@ template <int N>
 struct LoadBurst;  // N 16-byte stream loads + one metadata word, waited for together
 
 template <>
+struct LoadBurst<2> {
+  static __device__ __forceinline__ void run(u32x4 (&v)[2], uint32_t& w, const u32x4* const (&a)[2],
+                                             const uint32_t* am) {
+    asm volatile(BSR_LDX4(0, 3) BSR_LDX4(1, 4) BSR_LD1(2, 5) BSR_WAIT
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(w)
+                 : "v"(a[0]), "v"(a[1]), "v"(am)
+                 : "memory");
+  }
+};
+
+template <>
 struct LoadBurst<4> {
   static __device__ __forceinline__ void run(u32x4 (&v)[4], uint32_t& w, const u32x4* const (&a)[4],
                                              const uint32_t* am) {
     asm volatile(BSR_LDX4(0, 5) BSR_LDX4(1, 6) BSR_LDX4(2, 7) BSR_LDX4(3, 8) BSR_LD1(4, 9) BSR_WAIT
                  : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(w)
                  : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(am)
+                 : "memory");
+  }
+};
+
+template <>
+struct LoadBurst<5> {
+  static __device__ __forceinline__ void run(u32x4 (&v)[5], uint32_t& w, const u32x4* const (&a)[5],
+                                             const uint32_t* am) {
+    asm volatile(BSR_LDX4(0, 6) BSR_LDX4(1, 7) BSR_LDX4(2, 8) BSR_LDX4(3, 9) BSR_LDX4(4, 10) BSR_LD1(5, 11) BSR_WAIT
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(w)
+                 : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(am)
                  : "memory");
   }
 };
