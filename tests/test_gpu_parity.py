@@ -16,7 +16,7 @@ from gpu_side import GpuCase, say
 from oracle_side import build_case
 from paper_2608_17826_amd import bsr
 from workloads import generate, get_config
-from workloads.configs import Workload
+from workloads.configs import GroupSpec, Workload
 from workloads.gen import random_workload
 
 pytestmark = pytest.mark.gpu
@@ -483,5 +483,32 @@ def test_bind_refuses_prefixes_past_the_32_bit_token_range():
             bsr.bsr_request_bind(gc.ctx, 91, limit, [], 0, 0, 0, 0, 0)
         assert e.value.code == bsr.BSR_E_ARG and "2^32" not in str(e.value) and "NULL" in str(e.value)
         assert bsr.bsr_admission_get(gc.ctx)["n_bound"] == 0
+    finally:
+        gc.close()
+
+
+XCD_SPAN_LAYOUT = Workload(
+    index=200, name="xcd-span", n_tokens=34 * 16 + 5, chunk_tokens=16,
+    groups=(GroupSpec("c36", 16, 36, 512, value_kind="bytes"),), windows=(32,), pool_factor=2)
+
+
+@pytest.mark.parametrize("batch,grid", [(7, 252), (8, 288), (9, 324), (17, 612)])
+def test_xcd_work_order_spans_and_ragged_tail(batch, grid):
+    """The install issues its work items in runs across the XCDs for whole
+    spans of the grid and in plain order for the ragged rest.  One 8 KiB
+    piece per (tensor, chunk) gives 36 work items per chunk, so these batch
+    sizes make launches below one span, of exactly one span, and of one or
+    two spans plus a ragged tail (a span is 36 x the XCD count, 288 on
+    eight XCDs); every image must still equal the oracle's."""
+    wi = generate(XCD_SPAN_LAYOUT)
+    assert 36 * batch == grid
+    say(f"case: XCD spans, install batch {batch} (grid {grid})")
+    case, n, _, _, res = _oracle(wi, 32)
+    gc = GpuCase(wi, W=32, install_batch=batch)
+    try:
+        assert gc.probe(61)[0] == n == 34
+        out = gc.restore(61, n)
+        _compare_success(gc, case, res, out)
+        assert out.stats["n_install_launches"] == -(-n // batch)
     finally:
         gc.close()
