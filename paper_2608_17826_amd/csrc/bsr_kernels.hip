@@ -358,12 +358,12 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   // work index -> dispatch position (the group), then (chunk, piece within
   // the chunk's group range)
   const uint32_t bid = xcd_work_index(blockIdx.x, H.xcd_full, H.xcd_log2);
-  // Every wave of the workgroup runs this decode on the scalar unit, which
-  // the CU's waves share, so it is kept short: about 120 scalar instructions
-  // before the first data load (256 extra scalar instructions per wave cost
-  // a plain copy of this shape about 3 points of HBM bandwidth, 128 about
-  // 0.3).  The dispatch position is the count of group starts at or below
-  // bid (the starts increase with the position).
+  // Every wave runs this decode before its first data load, and that delay
+  // costs bandwidth, so it is kept short: about 120 scalar instructions
+  // (256 extra ones per wave cost a plain copy of this shape about 3 points
+  // of HBM bandwidth, 128 about 0.3).  The dispatch position is the count
+  // of group starts at or below bid (the starts increase with the
+  // position).
   uint32_t oi = 0;
 #pragma unroll
   for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) oi = add_if_ge(oi, bid, H.start[q]);
