@@ -408,8 +408,9 @@ int bsr_request_bind(bsr_ctx* ctx, uint64_t request_id, uint32_t n_hit_chunks,
  * install batch (which may span windows: chunks left over at the end of a
  * call join the next call's batch, and every later call of the request --
  * commit, invalidate, mark, end -- installs them first) it enqueues the
- * install and verify kernels on compute_stream and releases the batch's
- * slots behind them.  On a
+ * install kernel on compute_stream, releases the batch's slots behind it,
+ * then enqueues the verify kernel (which reads only the install's tag
+ * partials, not the slots).  On a
  * host-detected failure it enqueues the chunks before the failing one, then
  * an invalidate, and returns BSR_E_MISSING / BSR_E_TIMEOUT /
  * BSR_E_TRANSFER; later windows return BSR_E_STATE.  Device-detected

@@ -491,6 +491,12 @@ int flush_batch(bsr_ctx* c, Session& s) {
     return rc;
   }
   if (t0 && t1) s.timing.emplace_back(t0, t1);
+  // The batch's slots are free once the install has read them: the verify
+  // kernel reads only the tag partials, which the next install (later on
+  // this stream) overwrites after it.  Releasing here keeps the verify off
+  // the copy engine's path to the slots.
+  if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
+  for (uint32_t ch : chunks) s.slot_free_seq[ch % s.window] = seq;
   VerifyParams vp{};
   vp.partials = r.partials;
   vp.status = s.status;
@@ -503,8 +509,6 @@ int flush_batch(bsr_ctx* c, Session& s) {
   for (size_t i = 0; i < chunks.size(); ++i)
     for (uint32_t g = 0; g < BSR_MAX_GROUPS; ++g) vp.expected[i][g] = tags[i][g];
   if ((rc = hip_check(bsr::launch_verify(vp, s.compute), "verify launch"))) return rc;
-  if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
-  for (uint32_t ch : chunks) s.slot_free_seq[ch % s.window] = seq;
   s.st.n_install_launches++;
   s.st.installed_bytes += static_cast<uint64_t>(chunks.size()) * c->geo.chunk_payload;
   chunks.clear();
