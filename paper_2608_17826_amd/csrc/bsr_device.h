@@ -118,7 +118,8 @@ struct PackedDiv {
 inline PackedDiv pack_fastdiv(const FastDiv& f) { return PackedDiv{f.m, f.s1 | (f.s2 << 8)}; }
 
 #if defined(__HIP__)
-__device__ __forceinline__ uint32_t packed_div(uint32_t m, uint32_t s, uint32_t n) {
+// (host-callable too, so that a CPU test checks the kernel's own division)
+__host__ __device__ __forceinline__ uint32_t packed_div(uint32_t m, uint32_t s, uint32_t n) {
   const uint32_t t = static_cast<uint32_t>((static_cast<uint64_t>(m) * n) >> 32);
   return (t + ((n - t) >> (s & 0xffu))) >> (s >> 8);
 }
