@@ -420,7 +420,13 @@ int bsr_restore_window(bsr_ctx* ctx, uint64_t request_id, uint32_t first_chunk,
 
 /* Report group `group` of the bound request invalid outside any transfer
  * (its q_g of Eq. 6 becomes 0, e.g. the engine found an erroneous block in
- * that group).  Asynchronous, on compute_stream. */
+ * that group).  Asynchronous, on compute_stream, after the chunks already
+ * restored have been installed and verified (so a corruption among them is
+ * still the recorded failure).  From then on every later chunk is past the
+ * valid prefix: the device neither installs nor verifies it, and the commit
+ * falls back with fail = NONE and q_g = 0 unless an earlier failure was
+ * recorded.  Later windows are still accepted; their host-side checks
+ * (presence, deadline, transfer) still record the first such failure. */
 int bsr_mark_group_invalid(bsr_ctx* ctx, uint64_t request_id, uint32_t group);
 
 /* Request-level commit (Eq. 6 with one rank).  Enqueues the commit kernel:

@@ -44,5 +44,5 @@ from . import admission  # noqa: F401
 from .restore import (  # noqa: F401
     FAIL_NONE, FAIL_MISSING, FAIL_CORRUPT, FAIL_TIMEOUT, FAIL_TRANSFER, FAIL_ABORT,
     Runtime, RestoreResult, probe, plan_windows, live_trace, peak_live_staging,
-    windowed_restore, expected_block, request_blocks, set_request_valid,
+    windowed_restore, expected_block, request_blocks, set_request_valid, install_chunk,
 )

@@ -503,7 +503,13 @@ __global__ __launch_bounds__(kVerifyThreads) void k_verify(const VerifyParams p)
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint32_t pair = blockIdx.x;
   const uint32_t c = pair / p.n_groups, g = pair - c * p.n_groups;
-  const bool live = p.status->fail == 0;
+  // The install's own prefix test: with a failure recorded or some group
+  // already invalid (q_g = 0, e.g. reported by the engine between windows),
+  // the launch's chunks are past the valid prefix and installed nothing, so
+  // their partials are not compared (an empty partial is no corruption).
+  // Nothing writes the status words between an install and its verify.
+  bool live = p.status->fail == 0;
+  for (uint32_t gg = 0; gg < p.n_groups; ++gg) live = live && p.status->q[gg] != 0;
   uint32_t s = 0, x = 0;
   if (live) {
     const uint32_t lo = (c * p.wg_per_chunk + p.wg_start[g]) * kInstallWaves;

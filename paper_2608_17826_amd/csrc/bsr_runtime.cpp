@@ -333,8 +333,7 @@ struct Inject {
 };
 
 // Device and host resources of one session slot, allocated when the context
-// is created so that binding a request allocates nothing (whole-plan mode
-// grows its event vectors at bind).
+// is created so that binding a request allocates nothing.
 struct SessionRes {
   TagPair* partials = nullptr;            // per-wave tag partials of one install launch
   bsr::VerifyAux* verify_aux = nullptr;   // verify words
@@ -724,8 +723,10 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
     c->aux_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
     // event ring: the copy of chunk i waits for the release of chunk i - W,
-    // recorded at most W batches earlier (W + 2 leaves a margin); whole-plan
-    // contexts size it per request at bind
+    // recorded at most W batches earlier (W + 2 leaves a margin).  In
+    // whole-plan mode no slot is reused, so no copy waits for a release and
+    // two pairs serve any plan: a batch's copy event is waited for as soon
+    // as it is recorded, and a later record does not move an enqueued wait.
     const uint32_t E = W ? W + 2 : 2;
     bool ok = true;
     for (SessionRes& r : c->res) {
@@ -1156,20 +1157,6 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   fp.verify_aux = res.verify_aux;
   ip.h.partials = res.partials;
 
-  if (c->W == 0) {
-    // whole-plan mode: one event pair per install batch of the plan
-    const uint32_t E = (n_hit + c->batch - 1) / c->batch + 2;
-    while (res.full_ev.size() < E) {
-      hipEvent_t a = nullptr, b2 = nullptr;
-      if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess) return fail_with(BSR_E_NOMEM, "event creation failed");
-      if (hipEventCreateWithFlags(&b2, hipEventDisableTiming) != hipSuccess) {
-        (void)hipEventDestroy(a);
-        return fail_with(BSR_E_NOMEM, "event creation failed");
-      }
-      res.full_ev.push_back(a);
-      res.free_ev.push_back(b2);
-    }
-  }
   // begin: reset the status words and clear the advertised valid bytes
   FinishParams begin = fp;
   begin.mode = bsr::kFinishBegin;

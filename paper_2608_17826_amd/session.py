@@ -59,6 +59,11 @@ class RestoreSession:
         self.copy_stream = torch.cuda.Stream(device=self.device)
         self.compute_stream = torch.cuda.Stream(device=self.device)
 
+    def release_ring(self) -> None:
+        """Drop the ring; the next bind allocates it again."""
+        self.staging = None
+        self.staging_bytes = 0
+
     def _ring(self, nbytes: int) -> None:
         if self.staging is None or self.staging.numel() != nbytes:
             self.staging = None
@@ -82,10 +87,17 @@ class RestoreSession:
 
     def restore(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst],
                 plan: Optional[Sequence[Tuple[int, int]]] = None, abort_after_windows: Optional[int] = None,
-                before_commit=None) -> Outcome:
-        """bind, every window of the plan, then commit (or invalidate + commit)."""
+                before_commit=None, after_window=None, after_bind=None) -> Outcome:
+        """bind, every window of the plan, then commit (or invalidate + commit).
+
+        ``after_bind()`` and ``after_window(j)`` (once window j has been
+        enqueued) are the caller's hooks, e.g. a measurement, or an engine
+        reporting a group invalid mid-restore.
+        """
         torch.cuda.current_stream(self.device).synchronize()  # inputs written by torch are ready
         self.bind(request_id, n_hit, dsts)
+        if after_bind is not None:
+            after_bind()
         errors = []
         for j, (first, n) in enumerate(plan if plan is not None else self.windows(n_hit)):
             try:
@@ -93,6 +105,8 @@ class RestoreSession:
             except bsr.BsrError as e:
                 errors.append((first, e.code))
                 break
+            if after_window is not None:
+                after_window(j)
             if abort_after_windows is not None and j + 1 >= abort_after_windows:
                 bsr.bsr_invalidate(self.ctx, request_id, bsr.BSR_FAIL_ABORT)
                 break

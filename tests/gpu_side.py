@@ -91,3 +91,31 @@ class GpuCase:
 
     def close(self) -> None:
         bsr.bsr_ctx_destroy(self.ctx)
+
+
+def measured_restore(gc: GpuCase, request_id: int, n_hit: int, **kw):
+    """Restore one request with Eq. 1 measured across it.
+
+    The ring is dropped and allocated again by the bind, inside the measured
+    region, after the pools and the status block.  Returns the outcome and
+    {"peak_alloc_delta": growth of torch's peak allocated bytes from before
+    the ring to after the commit, "free_after_bind" / "free_after_commit":
+    the device's free bytes (hipMemGetInfo)}: a restore that allocates
+    nothing but its ring grows the peak by exactly the ring and leaves the
+    free bytes unchanged from bind to commit.
+    """
+    gc.session.release_ring()
+    torch.cuda.synchronize()
+    # the ring then takes a fresh segment, split exactly to its size (torch
+    # rounds segments to 2 MiB and splits off a remainder above 1 MiB)
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    m = {}
+
+    def after_bind():
+        m["free_after_bind"] = torch.cuda.mem_get_info()[0]
+    out = gc.restore(request_id, n_hit, after_bind=after_bind, **kw)
+    m["free_after_commit"] = torch.cuda.mem_get_info()[0]
+    m["peak_alloc_delta"] = torch.cuda.max_memory_allocated() - base
+    return out, m

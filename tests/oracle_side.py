@@ -65,6 +65,10 @@ class GeneratorStore:
     def has(self, key: int, g: int) -> bool:
         return int(key) in self.index and (int(key), g) not in self.removed
 
+    def payload(self, key: int, g: int) -> np.ndarray:
+        """The entry's bytes alone (no tag computed)."""
+        return self.wi.payload(self.index[int(key)], g)
+
     def get(self, key: int, g: int):
         i = self.index[int(key)]
         p = self.wi.payload(i, g)

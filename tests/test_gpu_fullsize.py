@@ -4,19 +4,19 @@ Runs the workloads at their real sizes in the launch configuration bench.py
 times (W from the workload, install batch = the library default).  Checks:
   * the probe (every chunk key bit-exact, the prefix length);
   * every valid byte of every group against the oracle's commit rule;
-  * sampled destination blocks (advertised and not) against the oracle's
-    whole-plan definition of a block;
-  * a property that holds at any size: in every group, the sum and XOR of
-    all 32-bit words over the advertised blocks equal the sum and XOR of the
-    oracle's entry tags (a block holds a permutation of its tokens' record
-    words, planar or not);
-  * the staging law: the ring the library requires is W x chunk bytes, the
-    torch allocation delta of that ring equals it, and the library's peak
-    live staging counter equals it;
+  * every byte of every destination pool: the advertised blocks against the
+    oracle's install mapping of the prefix, and every other block against
+    its bytes from before the restore, streamed back in slices of about
+    1 GiB (``fullimage``); a few sampled blocks also against the oracle's
+    separate whole-plan definition of one block (``expected_block``);
+  * Eq. 1 measured across the restore: with the ring allocated inside the
+    measured region, torch's peak allocated bytes grow by exactly W x chunk
+    bytes, the device's free bytes do not change from bind to commit, and the
+    library's peak live staging counter equals W x chunk bytes;
   * failures: the oracle walks the same failing restore (into sink pools,
-    since contents are unspecified after a failure) and fixes exposure,
-    fallback, reason, first failed chunk, q_g and every valid byte; blocks
-    outside the prefix are sampled unchanged.
+    since request-block contents are unspecified after a failure) and fixes
+    exposure, fallback, reason, first failed chunk, q_g and every valid byte;
+    every byte of every block outside the prefix is compared unchanged.
 """
 
 import gc as pygc
@@ -27,10 +27,12 @@ import pytest
 import torch
 
 import oracle
-from gpu_side import GpuCase, say
-from oracle_side import GeneratorStore, SinkPools, oracle_layout
+from fullimage import compare_full_image, compare_untouched_blocks
+from gpu_side import GpuCase, measured_restore, say
+from oracle_side import GeneratorStore, SinkPools, build_case, oracle_layout
 from paper_2608_17826_amd import bsr
 from workloads import generate, get_config
+from workloads.configs import Workload
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
@@ -50,46 +52,6 @@ def _expected_valid(wi, layout, n, value):
     valid = [v.copy() for v in wi.valid_init]
     oracle.set_request_valid(layout, n, wi.block_tables, valid, value)
     return valid
-
-
-def _word_sum_xor(t: torch.Tensor):
-    w = t.reshape(-1).view(torch.int32)
-    s = int(w.sum(dtype=torch.int64).item()) & 0xFFFFFFFF
-    x = w.clone()
-    while x.numel() > 1:
-        if x.numel() % 2:
-            x = torch.cat([x, torch.zeros(1, dtype=x.dtype, device=x.device)])
-        h = x.numel() // 2
-        x = torch.bitwise_xor(x[:h], x[h:])
-    return s, int(x.item()) & 0xFFFFFFFF
-
-
-def _check_pool_tags(gc, wi, keys, n):
-    """Sum/XOR of all words over the advertised blocks == combination of the
-    oracle's entry tags, per group."""
-    layout = oracle_layout(wi)
-    store = GeneratorStore(wi, keys)
-
-    def tag(i_g):
-        return oracle.entry_tag(wi.payload(*i_g))
-
-    for g, spec in enumerate(wi.workload.groups):
-        nreq = oracle.request_blocks(n, wi.workload.chunk_tokens, spec.block_tokens)
-        assert (n * wi.workload.chunk_tokens) % spec.block_tokens == 0
-        with ThreadPoolExecutor(16) as ex:
-            tags = list(ex.map(tag, [(i, g) for i in range(n)]))
-        es = sum(t & 0xFFFFFFFF for t in tags) & 0xFFFFFFFF
-        ex_ = 0
-        for t in tags:
-            ex_ ^= t >> 32
-        idx = gc.dev.block_tables[g][:nreq].long()
-        gs, gx = 0, 0
-        for p in gc.dev.pools[g]:
-            s, x = _word_sum_xor(p.index_select(0, idx))
-            gs = (gs + s) & 0xFFFFFFFF
-            gx ^= x
-        assert (gs, gx) == (es, ex_), f"group {g}: pool words do not match the entry tags"
-    return store
 
 
 def _sample_blocks(gc, wi, keys, n, per_group=40, seed=0, store=None):
@@ -115,9 +77,16 @@ def _check_valid(gc, wi, expected):
         np.testing.assert_array_equal(gc.valid_host(g), expected[g], err_msg=f"valid bytes of group {g}")
 
 
+def _check_staging_measured(m, W, slot_bytes):
+    """Eq. 1 across the restore: the ring is the only device memory it adds."""
+    assert m["peak_alloc_delta"] == W * slot_bytes, m
+    assert m["free_after_commit"] == m["free_after_bind"], m
+
+
 @pytest.mark.parametrize("W", [8, 16, 32, 64])
 def test_128k_window_law_and_prefix(W):
-    """Workload 3: 75% of chunks held; peak staging = W x chunk bytes exactly."""
+    """Workload 3: 75% of chunks held; peak staging = W x chunk bytes exactly,
+    measured across the restore; every pool byte equals the oracle's."""
     say(f"case: workload 3 (128K, 384 of 512 held), W={W}")
     wi = generate(get_config(3))
     layout = oracle_layout(wi)
@@ -130,30 +99,26 @@ def test_128k_window_law_and_prefix(W):
         on, obm, _ = oracle.probe(ostore, wi.tokens, 256, wi.salt)
         assert n == on == 384
         np.testing.assert_array_equal(bm, obm)
-        # the ring alone, allocated as the session allocates it
-        need = bsr.bsr_staging_bytes(gc.layout, W)
-        m0 = torch.cuda.memory_allocated()
-        ring = torch.empty(need, dtype=torch.uint8, device="cuda")
-        delta = torch.cuda.memory_allocated() - m0
-        del ring
-        assert need == delta == W * layout.slot_bytes == W * 9_707_520
-        out = gc.restore(30 + W, n)
+        assert bsr.bsr_staging_bytes(gc.layout, W) == W * layout.slot_bytes == W * 9_707_520
+        out, m = measured_restore(gc, 30 + W, n)
         assert out.exposed_tokens == 384 * 256 == 98_304 and out.fallback == 0
+        _check_staging_measured(m, W, layout.slot_bytes)
         st = out.stats
         assert st["peak_live_staging_bytes"] == oracle.peak_live_staging(n, W, layout.slot_bytes) == W * 9_707_520
         assert st["h2d_bytes"] == n * layout.slot_bytes
         assert st["installed_bytes"] == n * layout.chunk_payload_bytes
         assert st["n_windows"] == len(oracle.plan_windows(n, W))
         _check_valid(gc, wi, _expected_valid(wi, layout, n, 1))
-        _sample_blocks(gc, wi, keys, n, per_group=24, seed=W, store=ostore)
-        if W == 32:
-            _check_pool_tags(gc, wi, keys, n)
+        compare_full_image(gc.dev.pools, wi, keys, n, store=ostore, log=say)
+        _sample_blocks(gc, wi, keys, n, per_group=8, seed=W, store=ostore)
     finally:
         _free(gc)
 
 
 @pytest.mark.parametrize("k", [4, 5])
 def test_512k_success(k):
+    """512K tokens, W = 32, full hit: every pool byte of every group (40 GB of
+    pools for workload 4, 67 GB for workload 5) equals the oracle's."""
     say(f"case: workload {k} (512K), W=32, full hit")
     wi = generate(get_config(k))
     layout = oracle_layout(wi)
@@ -162,15 +127,50 @@ def test_512k_success(k):
     try:
         n, bm, gkeys = gc.probe(40 + k)
         assert [int(x) for x in gkeys] == keys and n == 2048 and bm.all()
-        out = gc.restore(40 + k, n)
+        out, m = measured_restore(gc, 40 + k, n)
         assert out.window_errors == [] and out.fallback == 0 and out.exposed_tokens == 524_288
+        _check_staging_measured(m, 32, layout.slot_bytes)
         st = out.stats
         assert st["peak_live_staging_bytes"] == 32 * layout.slot_bytes
         assert st["h2d_bytes"] == n * layout.slot_bytes
         assert st["installed_bytes"] == n * layout.chunk_payload_bytes
         _check_valid(gc, wi, _expected_valid(wi, layout, n, 1))
-        store = _check_pool_tags(gc, wi, keys, n)
-        _sample_blocks(gc, wi, keys, n, per_group=32, seed=k, store=store)
+        store = GeneratorStore(wi, keys)
+        total = compare_full_image(gc.dev.pools, wi, keys, n, store=store, log=say)
+        say(f"  all {total} pool bytes equal the oracle's")
+        _sample_blocks(gc, wi, keys, n, per_group=8, seed=k, store=store)
+    finally:
+        _free(gc)
+
+
+def test_mtp_layout_64_chunks_full_image():
+    """The 4-group layout (MLA @64, planar index keys @128, sliding window
+    @32, MTP @64) at 64 chunks, W = 32 with the default 28-chunk install
+    batch (launches that span windows): the whole image, every valid byte and
+    the counters against the oracle's windowed restore into whole pools."""
+    w5 = get_config(5)
+    w = Workload(index=5, name="512k-mtp-64-chunks", n_tokens=64 * 256, chunk_tokens=256,
+                 groups=w5.groups, windows=(32,), base_records=w5.base_records)
+    wi = generate(w)
+    say("case: 4-group layout, 64 chunks, W=32, default install batch")
+    case = build_case(wi)
+    n, _, keys = oracle.probe(case.store, wi.tokens, 256, wi.salt)
+    res = oracle.windowed_restore(case.layout, case.store, keys, n, 32, wi.block_tables, case.pools, case.valid)
+    assert n == 64 and res.fallback == 0
+    gc = GpuCase(wi, W=32)
+    try:
+        assert gc.probe(45)[0] == n
+        out, m = measured_restore(gc, 45, n)
+        assert out.stats["install_batch"] == 28 and out.stats["n_install_launches"] == 3
+        assert out.exposed_tokens == res.exposed_tokens and out.fallback == 0
+        assert out.status["q"][:4] == res.q == [1, 1, 1, 1]
+        _check_staging_measured(m, 32, case.layout.slot_bytes)
+        st = out.stats
+        assert st["peak_live_staging_bytes"] == res.peak_live_staging_bytes == 32 * 16_404_480
+        assert st["h2d_bytes"] == res.h2d_bytes and st["installed_bytes"] == res.installed_bytes
+        for g in range(4):
+            np.testing.assert_array_equal(gc.valid_host(g), case.valid[g], err_msg=f"valid bytes of group {g}")
+            np.testing.assert_array_equal(gc.pool_host(g), case.pools[g], err_msg=f"pool of group {g}")
     finally:
         _free(gc)
 
@@ -233,14 +233,8 @@ def test_512k_group_a_fault_after_probe(mode):
         if mode == "missing":
             assert out.window_errors == [(f["chunk"] // 32 * 32, bsr.BSR_E_MISSING)]
         _check_valid(gc, wi, valid)
-        # blocks outside the advertised prefix keep their sentinels
-        rng = np.random.default_rng(7)
-        for g, spec in enumerate(wi.workload.groups):
-            others = np.setdiff1d(np.arange(wi.pool_blocks[g]), wi.block_tables[g])
-            for b in rng.choice(others, size=12, replace=False):
-                t = int(rng.integers(0, spec.n_tensors))
-                np.testing.assert_array_equal(gc.dev.pools[g][t][int(b)].cpu().numpy(),
-                                              wi.sentinel_block(g, t, int(b)))
+        # every block outside the advertised prefix keeps its bytes
+        compare_untouched_blocks(gc.dev.pools, wi, n, log=say)
         assert gc.probe(50)[0] == 0      # force-local until RUNNING admission or teardown
         bsr.bsr_request_end(gc.ctx, 50)
     finally:
@@ -275,6 +269,7 @@ def test_512k_mtp_group_missing_beyond_k(which):
         assert out.status["first_failed_chunk"] == k + 1
         assert out.status["q"][:4] == res.q
         _check_valid(gc, wi, valid)
+        compare_untouched_blocks(gc.dev.pools, wi, n, log=say)
         # re-admission: force-local reports zero, then after RUNNING the
         # probe finds exactly the surviving prefix of k+1 chunks
         assert gc.probe(60)[0] == 0

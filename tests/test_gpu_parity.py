@@ -346,6 +346,87 @@ def test_group_fault_collapses_all_groups_and_mark_invalid():
         gc.close()
 
 
+@pytest.mark.parametrize("after", [1, 2])
+def test_group_marked_invalid_between_windows(after):
+    """Eq. 6's q_g reported 0 by the engine after window ``after`` of four
+    (workload 2, W = 32, default batch of 28, so an install batch is still
+    pending when the mark arrives): the later chunks are past the valid prefix
+    and install nothing, and their empty tag partials are no corruption.  The
+    commit falls back with fail NONE, no failed chunk and q = [1, 0], as the
+    oracle's engine-reported invalid group gives."""
+    wi = generate(get_config(2))
+    say(f"case: workload 2 (32K), W=32, group 1 marked invalid after window {after} of 4")
+    case, n, _, _, res = _oracle(wi, 32, invalid_groups=[1])
+    assert n == 128 and res.fail_reason == oracle.FAIL_NONE and res.q == [1, 0]
+    assert res.first_failed_chunk == 0xFFFFFFFF
+    gc = GpuCase(wi, W=32)
+    try:
+        n_g = gc.probe(8)[0]
+        assert n_g == n
+
+        def mark(j):
+            if j + 1 == after:
+                bsr.bsr_mark_group_invalid(gc.ctx, 8, 1)
+        out = gc.restore(8, n_g, after_window=mark)
+        assert out.window_errors == []
+        _compare_failure(gc, case, res, out)
+        assert out.status["first_failed_chunk"] == 0xFFFFFFFF
+        assert gc.probe(8)[0] == 0      # the fallback sets the force-local marker
+    finally:
+        gc.close()
+
+
+def test_corruption_before_a_mark_stays_the_recorded_failure():
+    """A corrupt entry in window 0, then the engine marks group 0 invalid
+    after window 1: the corruption was verified before the mark and stays the
+    first failure (CORRUPT at its chunk, q = 0 for both groups), as in the
+    oracle given the same corrupt entry and invalid group."""
+    wi = generate(get_config(2))
+    k, g_bad, byte, mask = 5, 1, 777, 0x21
+    say(f"case: workload 2 (32K), W=32, group {g_bad} corrupt at chunk {k}, group 0 marked after window 1")
+    case, n, _, _, res = _oracle(wi, 32, mutate=lambda c, keys: c.store.corrupt(keys[k], g_bad, byte, mask),
+                                 invalid_groups=[0])
+    assert res.fail_reason == oracle.FAIL_CORRUPT and res.first_failed_chunk == k and res.q == [0, 0]
+    gc = GpuCase(wi, W=32)
+    try:
+        n_g, _, keys = gc.probe(9)
+        gc.corrupt(int(keys[k]), g_bad, byte, mask)
+        out = gc.restore(9, n_g, after_window=lambda j: j == 0 and bsr.bsr_mark_group_invalid(gc.ctx, 9, 0))
+        _compare_failure(gc, case, res, out)
+    finally:
+        gc.close()
+
+
+# the first twelve random layouts with at least two chunks (a window boundary)
+_MARK_SEEDS = [s for s in range(40) if random_workload(s).n_full_chunks >= 2][:12]
+
+
+@pytest.mark.parametrize("seed", _MARK_SEEDS)
+def test_random_layout_group_marked_mid_restore(seed):
+    """Random layouts: a seeded group is marked invalid after a seeded window
+    (never the last), with a seeded install batch."""
+    w = random_workload(seed)
+    rng = np.random.default_rng(900 + seed)
+    n_full = w.n_full_chunks
+    W = int(rng.integers(1, n_full))           # at least two windows
+    n_windows = -(-n_full // W)
+    after = int(rng.integers(1, n_windows))
+    g = int(rng.integers(0, len(w.groups)))
+    batch = int(rng.integers(1, W + 1))
+    wi = generate(w)
+    say(f"case: random layout seed={seed} W={W} batch={batch} group {g} marked after window {after} of {n_windows}")
+    case, n, _, _, res = _oracle(wi, W, invalid_groups=[g])
+    gc = GpuCase(wi, W=W, install_batch=batch)
+    try:
+        n_g = gc.probe(10)[0]
+        assert n_g == n == n_full
+        out = gc.restore(10, n_g, after_window=lambda j: j + 1 == after and bsr.bsr_mark_group_invalid(gc.ctx, 10, g))
+        assert out.window_errors == []
+        _compare_failure(gc, case, res, out)
+    finally:
+        gc.close()
+
+
 def _eight_group_workload():
     """BSR_MAX_GROUPS groups mixing planar and contiguous kinds and block sizes
     that divide the chunk, exceed it, or neither; a ragged token tail."""

@@ -100,6 +100,15 @@ class WorkloadInputs:
         ramp = (np.arange(self.block_bytes(g), dtype=np.int64) * SENTINEL_STRIDE)
         return ((int(self.sentinel_seed[g][t, b]) + ramp) & 0xFF).astype(np.uint8)
 
+    def sentinel_blocks(self, g: int, blocks: np.ndarray) -> np.ndarray:
+        """uint8 [n_tensors, len(blocks), block_bytes]: those pool blocks before restore."""
+        bb = self.block_bytes(g)
+        ramp = ((np.arange(bb, dtype=np.int64) * SENTINEL_STRIDE) & 0xFF).astype(np.uint8)
+        s = self.sentinel_seed[g][:, np.asarray(blocks, dtype=np.int64)]
+        out = np.empty(s.shape + (bb,), dtype=np.uint8)
+        np.add(s[:, :, None], ramp[None, None, :], out=out)  # uint8 add wraps
+        return out
+
     def sentinel_pool(self, g: int) -> np.ndarray:
         """uint8 [n_tensors, pool_blocks, block_bytes]: the pool before restore."""
         bb = self.block_bytes(g)
