@@ -103,7 +103,17 @@ def measured_restore(gc: GpuCase, request_id: int, n_hit: int, **kw):
     the device's free bytes (hipMemGetInfo)}: a restore that allocates
     nothing but its ring grows the peak by exactly the ring and leaves the
     free bytes unchanged from bind to commit.
+
+    The first restores of a process see the HIP runtime set up its queues
+    for the session's streams and grow its internal pools with the depth of
+    the work in flight (2-14 MiB of device memory measured, never again once
+    a restore of the same shape has run), so the same restore runs once
+    first, on the same streams, and the measured restore is the next.
     """
+    warm_id = request_id + (1 << 40)
+    if n_hit and gc.probe(warm_id)[0] >= n_hit:
+        gc.restore(warm_id, n_hit)
+        bsr.bsr_request_end(gc.ctx, warm_id)
     gc.session.release_ring()
     torch.cuda.synchronize()
     # the ring then takes a fresh segment, split exactly to its size (torch
