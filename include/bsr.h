@@ -66,6 +66,7 @@ extern "C" {
 #define BSR_MAX_GROUPS 8
 #define BSR_MAX_INSTALL_BATCH 32
 #define BSR_MAX_BOUND_REQUESTS 16 /* session slots of one context */
+#define BSR_STATIC_SCRATCH_BYTES (2u << 20) /* per-GPU scratch of bsr_ctx_create_static contexts */
 #define BSR_NO_CHUNK 0xFFFFFFFFu
 
 /* status codes */
@@ -278,6 +279,31 @@ int bsr_chunk_keys(uint64_t salt, const int32_t* tokens, uint64_t n_tokens,
  * its HIP events and O(W) device auxiliary state on that device; with -1 only
  * the store and probe are usable.  *out is NULL on failure. */
 int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out);
+
+/* For callers that cannot allocate device or pinned memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same context as bsr_ctx_create, except that it makes no device or pinned
+ * allocation.  It calls neither hipMalloc, hipHostMalloc, hipFree nor any
+ * other allocating routine of HIP; it does create the context's HIP events.
+ * Its one session slot's device scratch (the install kernel's tag partials
+ * and the verify words) lives in a static array of
+ * BSR_STATIC_SCRATCH_BYTES inside the library, one per GPU, held from the
+ * first such context on that GPU until the process ends.  The status
+ * mirror that commit reads back into is plain host memory of the context.
+ * Requirements: hip_device >= 0, staging_budget_bytes = 0 and
+ * max_bound_requests <= 1 (the bounded-retrieve lock), else BSR_E_ARG; the
+ * scratch of one install launch, install_batch x (workgroups per chunk) x
+ * 16 B plus 64 B of verify words, must fit the array, else BSR_E_ARG (lower
+ * install_batch).  Every request of such a context on a GPU uses that GPU's
+ * array, which keeps the last request's contents.  Each bind clears the
+ * verify words, and each install writes every partial its verify reads.
+ * Requests that overlapped on one GPU's array would race, so the library
+ * allows one such context per GPU per process at a time: a second
+ * bsr_ctx_create_static on the same device returns BSR_E_BUSY until the
+ * first is destroyed.  Pair it with bsr_store_adopt and a caller arena,
+ * because bsr_store_reserve allocates.  Destroy with bsr_ctx_destroy.  *out
+ * is NULL on failure. */
+int bsr_ctx_create_static(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out);
 
 /* Destroy a context: waits for outstanding device work of bound requests,
  * frees library-owned memory (arena, events, aux).  NULL is a no-op. */

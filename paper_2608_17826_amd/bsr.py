@@ -22,6 +22,7 @@ BSR_ABI_VERSION = 2
 BSR_MAX_GROUPS = 8
 BSR_MAX_INSTALL_BATCH = 32
 BSR_MAX_BOUND_REQUESTS = 16
+BSR_STATIC_SCRATCH_BYTES = 2 << 20
 BSR_NO_CHUNK = 0xFFFFFFFF
 
 BSR_OK = 0
@@ -111,6 +112,7 @@ def _load() -> ct.CDLL:
         "bsr_plan_staging_bytes": (U64, [VP, U32]),
         "bsr_chunk_keys": (ct.c_int, [U64, VP, U64, U32, VP]),
         "bsr_ctx_create": (ct.c_int, [P(bsr_layout), P(bsr_config), P(VP)]),
+        "bsr_ctx_create_static": (ct.c_int, [P(bsr_layout), P(bsr_config), P(VP)]),
         "bsr_ctx_destroy": (ct.c_int, [VP]),
         "bsr_store_reserve": (ct.c_int, [VP, U64]),
         "bsr_store_adopt": (ct.c_int, [VP, VP, U64]),
@@ -233,6 +235,16 @@ def bsr_ctx_create(layout: bsr_layout, window_chunks: int, hip_device: int = 0,
     out = ct.c_void_p()
     _check(_lib.bsr_ctx_create(ct.byref(layout), ct.byref(cfg), ct.byref(out)))
     return Ctx(out.value, layout, window_chunks, staging_budget_bytes)
+
+
+def bsr_ctx_create_static(layout: bsr_layout, window_chunks: int, hip_device: int = 0,
+                          install_batch: int = 0, flags: int = 0, window_timeout_ms: int = 0) -> Ctx:
+    """A context whose device scratch is the library's static per-GPU array
+    (no device or pinned allocation); one session slot."""
+    cfg = bsr_config(window_chunks, install_batch, hip_device, flags, window_timeout_ms, 0, 0)
+    out = ct.c_void_p()
+    _check(_lib.bsr_ctx_create_static(ct.byref(layout), ct.byref(cfg), ct.byref(out)))
+    return Ctx(out.value, layout, window_chunks, 0)
 
 
 def bsr_ctx_destroy(ctx: Ctx) -> None:

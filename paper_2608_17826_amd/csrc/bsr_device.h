@@ -264,6 +264,17 @@ struct FinishParams {
   GroupValid g[BSR_MAX_GROUPS];
 };
 
+// Scratch of a context that allocates nothing (bsr_ctx_create_static): one
+// array per GPU in the library's code object, holding one session slot's
+// install tag partials and verify words.  static_scratch_claim runs at the
+// context's set-up with `device` current: the first claim on a device looks
+// the array's device address up (hipGetSymbolAddress) and keeps it; a claim
+// while another context of this process holds the device's array sets *busy.
+constexpr uint64_t kStaticScratchBytes = BSR_STATIC_SCRATCH_BYTES;
+constexpr int kMaxScratchDevices = 64;
+hipError_t static_scratch_claim(int device, void** ptr, bool* busy);
+void static_scratch_release(int device);
+
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s,
                           hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_verify(const VerifyParams& p, hipStream_t s);

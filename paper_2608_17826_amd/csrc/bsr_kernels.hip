@@ -27,6 +27,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "bsr_device.h"
 
 #ifndef BSR_UNROLL
@@ -637,6 +639,44 @@ __global__ __launch_bounds__(256) void k_finish(const FinishParams p) {
     const int32_t b = p.g[g].block_table[k];
     if (b >= 0 && static_cast<uint32_t>(b) < p.g[g].pool_blocks) p.g[g].valid[b] = value;
   }
+}
+
+// The static scratch.  In host code `scratch` names a host-side stand-in,
+// not device memory: only the address from hipGetSymbolAddress, taken per
+// device with that device current, is ever passed to a kernel or a copy.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+bool g_scratch_claimed[kMaxScratchDevices] = {};
+}  // namespace
+
+hipError_t static_scratch_claim(int device, void** ptr, bool* busy) {
+  *ptr = nullptr;
+  *busy = false;
+  if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_claimed[device]) {
+    *busy = true;
+    return hipSuccess;
+  }
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[device] = p;
+  }
+  g_scratch_claimed[device] = true;
+  *ptr = g_scratch_ptr[device];
+  return hipSuccess;
+}
+
+void static_scratch_release(int device) {
+  if (device < 0 || device >= kMaxScratchDevices) return;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  g_scratch_claimed[device] = false;
 }
 
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s, hipEvent_t start,

@@ -340,6 +340,11 @@ struct SessionRes {
   bsr_dev_status* host_status = nullptr;  // pinned mirror of the status block
   std::vector<hipEvent_t> full_ev, free_ev;
   bool in_use = false;
+  // A context that allocates nothing: partials and verify words are in the
+  // library's static array, and the status mirror is status_buf (plain host
+  // memory; the readback waits for the stream anyway).
+  bool static_scratch = false;
+  bsr_dev_status status_buf{};
 };
 
 struct Session {  // one bound request
@@ -398,6 +403,7 @@ struct bsr_ctx {
   uint64_t aux_bytes = 0;       // device bytes per session slot
   uint32_t xcd_log2 = 3;        // log2 of the XCDs of the device's partition
   std::vector<hipEvent_t> timing_pool;
+  bool static_claimed = false;  // holds its device's static scratch array
 };
 
 namespace {
@@ -614,15 +620,17 @@ static void free_session_res(SessionRes& r) {
     if (e) (void)hipEventDestroy(e);
   r.full_ev.clear();
   r.free_ev.clear();
-  if (r.partials) (void)hipFree(r.partials);
-  if (r.verify_aux) (void)hipFree(r.verify_aux);
-  if (r.host_status) (void)hipHostFree(r.host_status);
+  if (!r.static_scratch) {
+    if (r.partials) (void)hipFree(r.partials);
+    if (r.verify_aux) (void)hipFree(r.verify_aux);
+    if (r.host_status) (void)hipHostFree(r.host_status);
+  }
   r.partials = nullptr;
   r.verify_aux = nullptr;
   r.host_status = nullptr;
 }
 
-int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out) {
+static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out, bool static_scratch) {
   if (!out) return fail_with(BSR_E_ARG, "out is NULL");
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
@@ -651,6 +659,9 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
     return fail_with(BSR_E_ARG, "max_bound_requests %u exceeds %d", M, BSR_MAX_BOUND_REQUESTS);
   const uint64_t slot_bytes = bsr_slot_bytes(layout);
   const uint64_t min_ring = static_cast<uint64_t>(std::max(W, 1u)) * slot_bytes;
+  if (static_scratch && (B != 0 || M > 1 || config->hip_device < 0))
+    return fail_with(BSR_E_ARG, "a context without allocations has one session slot on a GPU: "
+                                "staging_budget_bytes = 0, max_bound_requests <= 1, hip_device >= 0");
   if (B == 0) {
     if (M > 1) return fail_with(BSR_E_ARG, "max_bound_requests %u needs a staging budget (bounded-retrieve lock: 1)", M);
     M = 1;
@@ -721,7 +732,31 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
     else
       (void)hipGetLastError();
     c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
-    c->aux_bytes = c->partials_bytes + sizeof(bsr::VerifyAux);
+    c->aux_bytes = align_up(c->partials_bytes, kAlign) + sizeof(bsr::VerifyAux);
+    uint8_t* scratch = nullptr;
+    if (static_scratch) {
+      if (c->aux_bytes > bsr::kStaticScratchBytes) {
+        const uint64_t need = c->aux_bytes;
+        delete c;
+        return fail_with(BSR_E_ARG,
+                         "install launches of %u chunks need %llu B of scratch; the static array holds %llu B "
+                         "(lower install_batch)",
+                         b, (unsigned long long)need, (unsigned long long)bsr::kStaticScratchBytes);
+      }
+      void* p = nullptr;
+      bool busy = false;
+      if ((rc = hip_check(bsr::static_scratch_claim(c->device, &p, &busy), "hipGetSymbolAddress(scratch)"))) {
+        delete c;
+        return rc;
+      }
+      if (busy) {
+        delete c;
+        return fail_with(BSR_E_BUSY, "another context of this process holds device %d's static scratch",
+                         config->hip_device);
+      }
+      c->static_claimed = true;
+      scratch = static_cast<uint8_t*>(p);
+    }
     // event ring: the copy of chunk i waits for the release of chunk i - W,
     // recorded at most W batches earlier (W + 2 leaves a margin).  In
     // whole-plan mode no slot is reused, so no copy waits for a release and
@@ -732,9 +767,16 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
     for (SessionRes& r : c->res) {
       r.full_ev.assign(E, nullptr);
       r.free_ev.assign(E, nullptr);
-      ok = ok && hipMalloc(reinterpret_cast<void**>(&r.partials), c->partials_bytes) == hipSuccess &&
-           hipMalloc(reinterpret_cast<void**>(&r.verify_aux), sizeof(bsr::VerifyAux)) == hipSuccess &&
-           hipHostMalloc(reinterpret_cast<void**>(&r.host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
+      if (scratch) {  // the one session slot of a context without allocations
+        r.static_scratch = true;
+        r.partials = reinterpret_cast<TagPair*>(scratch);
+        r.verify_aux = reinterpret_cast<bsr::VerifyAux*>(scratch + align_up(c->partials_bytes, kAlign));
+        r.host_status = &r.status_buf;
+      } else {
+        ok = ok && hipMalloc(reinterpret_cast<void**>(&r.partials), c->partials_bytes) == hipSuccess &&
+             hipMalloc(reinterpret_cast<void**>(&r.verify_aux), sizeof(bsr::VerifyAux)) == hipSuccess &&
+             hipHostMalloc(reinterpret_cast<void**>(&r.host_status), sizeof(bsr_dev_status), hipHostMallocDefault) == hipSuccess;
+      }
       for (uint32_t i = 0; ok && i < E; ++i)
         ok = hipEventCreateWithFlags(&r.full_ev[i], hipEventDisableTiming) == hipSuccess &&
              hipEventCreateWithFlags(&r.free_ev[i], hipEventDisableTiming) == hipSuccess;
@@ -747,6 +789,14 @@ int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx**
   }
   *out = c;
   return BSR_OK;
+}
+
+int bsr_ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out) {
+  return ctx_create(layout, config, out, false);
+}
+
+int bsr_ctx_create_static(const bsr_layout* layout, const bsr_config* config, bsr_ctx** out) {
+  return ctx_create(layout, config, out, true);
 }
 
 
@@ -765,6 +815,7 @@ int bsr_ctx_destroy(bsr_ctx* c) {
       }
     }
     for (SessionRes& r : c->res) free_session_res(r);
+    if (c->static_claimed) bsr::static_scratch_release(c->device);
     for (auto e : c->timing_pool) (void)hipEventDestroy(e);
     if (c->store.owned && c->store.arena) (void)hipHostFree(c->store.arena);
   }

@@ -136,6 +136,12 @@ int main(int argc, char** argv) {
   CHECK(bsr_ctx_create(&L, &cfg, &ctx) == BSR_OK);
   CHECK(bsr_admission_get(ctx, &adm) == BSR_OK && adm.max_bound_requests == 5);
   CHECK(bsr_ctx_destroy(ctx) == BSR_OK);
+  /* a context without allocations: one session slot on a GPU only */
+  ctx = (bsr_ctx*)1;
+  CHECK(bsr_ctx_create_static(&L, &cfg, &ctx) == BSR_E_ARG && ctx == NULL); /* budget set */
+  cfg.staging_budget_bytes = 0;
+  ctx = (bsr_ctx*)1;
+  CHECK(bsr_ctx_create_static(&L, &cfg, &ctx) == BSR_E_ARG && ctx == NULL); /* hip_device = -1 */
   L.groups[1].split_bytes = 36; /* split must be < record */
   CHECK(bsr_slot_bytes(&L) == 0);
   free(arena);

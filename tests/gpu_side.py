@@ -34,17 +34,26 @@ class GpuCase:
 
     def __init__(self, wi: WorkloadInputs, W: int, install_batch: int = 0, flags: int = 0,
                  timeout_ms: int = 0, held: Optional[int] = None, device: str = "cuda:0",
-                 pinned_chunks=None, arena_chunks: Optional[int] = None):
+                 pinned_chunks=None, arena_chunks: Optional[int] = None, static: bool = False):
+        """``static``: a context that allocates nothing (bsr_ctx_create_static),
+        its store in a pinned arena the test allocates and adopts."""
         self.wi = wi
         w = wi.workload
         self.layout = layout_of(wi)
-        self.ctx = bsr.bsr_ctx_create(self.layout, W, hip_device=0, install_batch=install_batch,
-                                      flags=flags, window_timeout_ms=timeout_ms)
+        create = bsr.bsr_ctx_create_static if static else bsr.bsr_ctx_create
+        self.ctx = create(self.layout, W, hip_device=0, install_batch=install_batch,
+                          flags=flags, window_timeout_ms=timeout_ms)
         held = w.held_chunks if held is None else held
         chunks = list(range(held)) if pinned_chunks is None else list(pinned_chunks)
         slot = bsr.bsr_slot_bytes(self.layout)
         stride = (slot + 4095) // 4096 * 4096
-        bsr.bsr_store_reserve(self.ctx, stride * ((len(chunks) if arena_chunks is None else arena_chunks) + 2))
+        arena_bytes = stride * ((len(chunks) if arena_chunks is None else arena_chunks) + 2)
+        self.arena = None
+        if static:
+            self.arena = torch.empty(arena_bytes, dtype=torch.uint8, pin_memory=True)
+            bsr.bsr_store_adopt(self.ctx, self.arena.data_ptr(), arena_bytes)
+        else:
+            bsr.bsr_store_reserve(self.ctx, arena_bytes)
         self.keys = bsr.bsr_chunk_keys(wi.salt, wi.tokens, w.chunk_tokens)
         self._put(chunks)
         self.dev = place(wi, device)
