@@ -104,6 +104,12 @@ extern "C" {
                                       id outside [0, pool_blocks) fails the request (fail = BSR_FAIL_BLOCK_TABLE,
                                       nothing exposed; the kernels never write such an id).  The caller
                                       guarantees that no id repeats within one group's prefix (not checked) */
+#define BSR_FLAG_SDMA_COPIES 4u   /* stage chunks with the copy engine (hipMemcpyAsync) instead of the
+                                      library's staging-copy kernel.  By default a small kernel on the copy
+                                      stream reads each run of chunks from pinned host memory (the library's
+                                      arena, an adopted arena that HIP reports pinned over its whole range,
+                                      or the file tier's bounce buffers) into the ring; a source HIP does not
+                                      report pinned is always copied by the copy engine */
 
 /* fault injection (bsr_debug_inject), forced from the host */
 #define BSR_INJECT_NONE 0
@@ -147,9 +153,9 @@ typedef struct bsr_config {
   uint32_t window_chunks;     /* W: staging slots, the restore-window size; 0 = legacy whole-plan mode
                                  (§4 "Restore-window configuration": each request's ring holds its whole
                                  plan, n_hit slots, none reused; peak staging n_hit * slot bytes, Eq. 2) */
-  uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W up to W = 8, else W - W/8;
-                                 at most BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
-                                 windows; a batch smaller than W keeps the copy engine busy across windows.
+  uint32_t install_batch;     /* chunks per install launch, 0 = automatic (W - max(1, W/8), at least 1, at
+                                 most BSR_MAX_INSTALL_BATCH); <= min(W, BSR_MAX_INSTALL_BATCH).  Batches may span
+                                 windows; a batch smaller than W keeps the staging copies going across windows.
                                  BSR_E_ARG when one launch of this many chunks would exceed HIP's 2^32 - 1
                                  work-items (a layout of very many small tensors): lower it */
   int32_t hip_device;         /* HIP device ordinal; -1 = host-only context (store + probe only) */
@@ -508,6 +514,12 @@ int bsr_debug_inject(bsr_ctx* ctx, int32_t kind, uint32_t chunk, uint32_t param)
  * 1e9 B/s.  Needs a GPU context. */
 int bsr_measure_h2d(bsr_ctx* ctx, uint64_t bytes, uint32_t n_streams, uint32_t reps,
                     double* gbps);
+
+/* The same link measured with the library's staging-copy kernel: best of
+ * `reps` timed launches reading `bytes` (a multiple of 16) from a fresh
+ * hipHostMalloc buffer into device memory.  *gbps in 1e9 B/s.  Needs a GPU
+ * context. */
+int bsr_measure_stage(bsr_ctx* ctx, uint64_t bytes, uint32_t reps, double* gbps);
 
 #ifdef __cplusplus
 }

@@ -33,7 +33,7 @@ BSR_FAIL_NONE, BSR_FAIL_MISSING, BSR_FAIL_CORRUPT = 0, 1, 2
 BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT, BSR_FAIL_BLOCK_TABLE = 3, 4, 5, 6
 
 BSR_KIND_CONTIG, BSR_KIND_PLANAR = 0, 1
-BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES = 1, 2
+BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES, BSR_FLAG_SDMA_COPIES = 1, 2, 4
 BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR, BSR_INJECT_LAUNCH_ERROR = 0, 1, 2, 3
 BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
 BSR_FILE_DIRECT = 1
@@ -134,6 +134,7 @@ def _load() -> ct.CDLL:
         "bsr_admission_get": (ct.c_int, [VP, P(bsr_admission)]),
         "bsr_debug_inject": (ct.c_int, [VP, I32, U32, U32]),
         "bsr_measure_h2d": (ct.c_int, [VP, U64, U32, U32, P(ct.c_double)]),
+        "bsr_measure_stage": (ct.c_int, [VP, U64, U32, P(ct.c_double)]),
         "bsr_file_tier_open": (ct.c_int, [VP, ct.c_char_p, U32, U32, U32]),
         "bsr_file_tier_put_chunk": (ct.c_int, [VP, U64, P(VP)]),
         "bsr_file_tier_remove": (ct.c_int, [VP, U64, I32]),
@@ -371,6 +372,12 @@ def bsr_debug_inject(ctx: Ctx, kind: int, chunk: int = 0, param: int = 0) -> Non
 def bsr_measure_h2d(ctx: Ctx, nbytes: int, n_streams: int = 1, reps: int = 10) -> float:
     g = ct.c_double()
     _check(_lib.bsr_measure_h2d(ctx, nbytes, n_streams, reps, ct.byref(g)))
+    return g.value
+
+
+def bsr_measure_stage(ctx: Ctx, nbytes: int, reps: int = 10) -> float:
+    g = ct.c_double()
+    _check(_lib.bsr_measure_stage(ctx, nbytes, reps, ct.byref(g)))
     return g.value
 
 

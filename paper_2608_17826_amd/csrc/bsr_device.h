@@ -264,6 +264,33 @@ struct FinishParams {
   GroupValid g[BSR_MAX_GROUPS];
 };
 
+// Staging copy (pinned host memory -> ring slot) done by a kernel on the
+// copy stream instead of the copy engine.  src is the device's view of the
+// pinned source, 16-byte aligned; dst is in the ring, 16-byte aligned; bytes
+// is a multiple of 4.  The host checks both ranges before every launch.
+struct StageParams {
+  const uint8_t* src;
+  uint8_t* dst;
+  uint64_t bytes;
+};
+// Shape: the host link needs about its bandwidth-delay product in flight,
+// and reads queued beyond it delay the install's HBM traffic.  32
+// workgroups x 256 threads x 2 vectors keep 256 KiB in flight: 57.6 GB/s
+// from pinned memory, and installs that overlap the copy run as fast as
+// alone (154 us per 28-chunk launch at the 512K 4-group workload).  Measured
+// in the restore (grid x vectors: link GB/s, W = 32 install us): 64 x 4
+// (1 MiB in flight) 57.5, 468; 32 x 4: 56.9, 200; 24 x 4: 55.5, 173;
+// 64 x 1: 57.6, 161; 16 x 4: 57.2, 156; 8 x 8: 57.3, 150.
+#ifndef BSR_STAGE_GRID
+#define BSR_STAGE_GRID 32
+#endif
+#ifndef BSR_STAGE_UNROLL
+#define BSR_STAGE_UNROLL 2
+#endif
+constexpr int kStageThreads = 256;
+constexpr int kStageUnroll = BSR_STAGE_UNROLL;  // 16-byte vectors in flight per thread
+constexpr int kStageMaxGrid = BSR_STAGE_GRID;   // workgroups
+
 // Scratch of a context that allocates nothing (bsr_ctx_create_static): one
 // array per GPU in the library's code object, holding one session slot's
 // install tag partials and verify words.  static_scratch_claim runs at the
@@ -278,6 +305,7 @@ void static_scratch_release(int device);
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s,
                           hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_verify(const VerifyParams& p, hipStream_t s);
+hipError_t launch_stage(const StageParams& p, hipStream_t s);
 hipError_t launch_finish(const FinishParams& p, hipStream_t s);
 
 }  // namespace bsr

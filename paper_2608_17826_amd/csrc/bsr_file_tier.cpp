@@ -131,6 +131,7 @@ int FileTier::start(int device, std::string* err) {
   if (started_) return 0;
   device_ = device;
   bounce_.assign(readahead_, nullptr);
+  bounce_dev_.assign(readahead_, nullptr);
   bounce_ev_.assign(readahead_, nullptr);
   slots_.assign(readahead_, Slot{});
   for (uint32_t b = 0; b < readahead_; ++b) {
@@ -138,6 +139,9 @@ int FileTier::start(int device, std::string* err) {
     const bool ok = hipHostMalloc(&p, file_bytes_, hipHostMallocDefault) == hipSuccess &&
                     hipEventCreateWithFlags(&bounce_ev_[b], hipEventDisableTiming) == hipSuccess;
     bounce_[b] = static_cast<uint8_t*>(p);
+    void* dv = nullptr;
+    if (ok && hipHostGetDevicePointer(&dv, p, 0) == hipSuccess) bounce_dev_[b] = static_cast<const uint8_t*>(dv);
+    else (void)hipGetLastError();
     if (!ok) {
       *err = "file tier: bounce buffers could not be allocated";
       for (uint32_t k = 0; k <= b; ++k) {
@@ -145,6 +149,7 @@ int FileTier::start(int device, std::string* err) {
         if (bounce_[k]) (void)hipHostFree(bounce_[k]);
       }
       bounce_.clear();
+      bounce_dev_.clear();
       bounce_ev_.clear();
       return -1;
     }
@@ -171,6 +176,7 @@ void FileTier::close() {
     for (auto p : bounce_)
       if (p) (void)hipHostFree(p);
     bounce_.clear();
+    bounce_dev_.clear();
     bounce_ev_.clear();
     started_ = false;
   }

@@ -57,6 +57,10 @@ class FileTier {
   uint32_t pool_size() const { return readahead_; }
   uint64_t bounce_bytes() const { return static_cast<uint64_t>(readahead_) * file_bytes_; }
   const uint8_t* bounce_data(uint32_t b) const { return bounce_[b] + kHeaderBytes; }
+  // the whole pinned buffer b (header and body) and the device's view of it
+  const uint8_t* bounce_base(uint32_t b) const { return bounce_[b]; }
+  const uint8_t* bounce_device(uint32_t b) const { return bounce_dev_[b]; }
+  uint64_t file_bytes() const { return file_bytes_; }
   hipEvent_t bounce_event(uint32_t b) const { return bounce_ev_[b]; }
   // Queue a read of key's file into bounce buffer b.  The reader first waits
   // for bounce_event(b), i.e. for the last device copy out of that buffer.
@@ -111,6 +115,7 @@ class FileTier {
   bool started_ = false;
   std::vector<Slot> slots_;
   std::vector<uint8_t*> bounce_;
+  std::vector<const uint8_t*> bounce_dev_;  // device views of the bounce buffers (null: copy engine only)
   std::vector<hipEvent_t> bounce_ev_;
   std::vector<std::thread> workers_;
 };

@@ -27,6 +27,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "bsr_device.h"
@@ -36,6 +37,9 @@
 #endif
 #ifndef BSR_NT_LOAD
 #define BSR_NT_LOAD 1   // staged chunks are read once: non-temporal loads
+#endif
+#ifndef BSR_STAGE_NT_STORE
+#define BSR_STAGE_NT_STORE 0  // staging-copy stores: 1 non-temporal, 0 ordinary
 #endif
 
 
@@ -641,6 +645,44 @@ __global__ __launch_bounds__(256) void k_finish(const FinishParams p) {
   }
 }
 
+// Staging copy: pinned host memory (the device's view of it) into a ring
+// slot, read over the host link by a small grid (kStageMaxGrid workgroups,
+// kStageUnroll 16-byte loads in flight per thread before its stores).  The
+// stores are ordinary: the install reads the slot next, and non-temporal
+// stores made overlapping installs slower (16 x 4 at W = 32: 167 against
+// 155 us per launch).  Compared with the copy engine (hipMemcpyAsync), a
+// kernel's completion hands over to the install on the compute stream
+// sooner, which is most of what a small window lost per window.
+__global__ __launch_bounds__(kStageThreads) void k_stage(const StageParams p) {
+  const u32x4* __restrict__ s4 = reinterpret_cast<const u32x4*>(p.src);
+  u32x4* __restrict__ d4 = reinterpret_cast<u32x4*>(p.dst);
+  const uint64_t nvec = p.bytes >> 4;
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kStageThreads;
+  for (uint64_t base = static_cast<uint64_t>(blockIdx.x) * kStageThreads + threadIdx.x; base < nvec;
+       base += stride * kStageUnroll) {
+    u32x4 v[kStageUnroll];
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const uint64_t i = base + u * stride;
+      if (i < nvec) v[u] = *global_ptr(s4 + i);
+    }
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const uint64_t i = base + u * stride;
+#if BSR_STAGE_NT_STORE
+      if (i < nvec) __builtin_nontemporal_store(v[u], global_ptr(d4 + i));
+#else
+      if (i < nvec) *global_ptr(d4 + i) = v[u];
+#endif
+    }
+  }
+  // a tail of up to three words
+  const uint64_t w0 = nvec * 4, nw = p.bytes >> 2;
+  if (blockIdx.x == 0 && w0 + threadIdx.x < nw)
+    *global_ptr(reinterpret_cast<uint32_t*>(p.dst) + w0 + threadIdx.x) =
+        *global_ptr(reinterpret_cast<const uint32_t*>(p.src) + w0 + threadIdx.x);
+}
+
 // The static scratch.  In host code `scratch` names a host-side stand-in,
 // not device memory: only the address from hipGetSymbolAddress, taken per
 // device with that device current, is ever passed to a kernel or a copy.
@@ -689,6 +731,16 @@ hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStre
   } else {
     hipLaunchKernelGGL(k_install, dim3(n_workgroups), dim3(kInstallThreads), p.h.lds_bytes, s, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_stage(const StageParams& p, hipStream_t s) {
+  if (((reinterpret_cast<uintptr_t>(p.src) | reinterpret_cast<uintptr_t>(p.dst)) & 15u) || (p.bytes & 3u))
+    return hipErrorInvalidValue;
+  if (p.bytes == 0) return hipSuccess;
+  const uint64_t per_wg = static_cast<uint64_t>(kStageThreads) * kStageUnroll * 16;
+  const uint64_t grid = std::min<uint64_t>(kStageMaxGrid, (p.bytes + per_wg - 1) / per_wg);
+  hipLaunchKernelGGL(k_stage, dim3(static_cast<uint32_t>(grid)), dim3(kStageThreads), 0, s, p);
   return hipGetLastError();
 }
 

@@ -276,6 +276,9 @@ struct Store {
   uint8_t* arena = nullptr;
   uint64_t arena_bytes = 0;
   bool owned = false;
+  // the device's view of the arena when HIP reports it pinned over its whole
+  // range (the staging-copy kernel reads it); null: the copy engine copies
+  const uint8_t* arena_dev = nullptr;
   uint64_t block_stride = 0;
   uint32_t n_blocks = 0;
   std::vector<BlockMeta> meta;
@@ -404,6 +407,7 @@ struct bsr_ctx {
   uint32_t xcd_log2 = 3;        // log2 of the XCDs of the device's partition
   std::vector<hipEvent_t> timing_pool;
   bool static_claimed = false;  // holds its device's static scratch array
+  bool kernel_copies = true;    // staging copies by k_stage (else the copy engine)
 };
 
 namespace {
@@ -450,6 +454,24 @@ int find_active(bsr_ctx* c, uint64_t request_id, Session** out) {
   if (s->completing) return fail_with(BSR_E_STATE, "request %llu is being completed", (unsigned long long)request_id);
   *out = s;
   return BSR_OK;
+}
+
+// A staging copy of `bytes` from host memory `src` into the ring at `dst`, on
+// the copy stream.  When the source lies in a pinned allocation
+// [base, base + extent) whose device view is `dev`, k_stage reads it over
+// the host link; otherwise (or with BSR_FLAG_SDMA_COPIES) the copy engine
+// copies it.  Both ranges are checked here before any kernel is launched:
+// the source inside its pinned allocation, the destination inside this
+// request's ring.
+hipError_t stage_copy(bsr_ctx* c, Session& s, uint8_t* dst, const uint8_t* src, uint64_t bytes, const uint8_t* base,
+                      const uint8_t* dev, uint64_t extent) {
+  if (!c->kernel_copies || !dev || !base)
+    return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s.copy);
+  const bool src_in = src >= base && bytes <= extent && static_cast<uint64_t>(src - base) <= extent - bytes;
+  const bool dst_in = dst >= s.staging && bytes <= s.ring_bytes &&
+                      static_cast<uint64_t>(dst - s.staging) <= s.ring_bytes - bytes;
+  if (!src_in || !dst_in) return hipErrorInvalidValue;
+  return bsr::launch_stage(bsr::StageParams{dev + (src - base), dst, bytes}, s.copy);
 }
 
 // Enqueue install + verify for the chunks staged since the last flush.
@@ -635,20 +657,22 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
-  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES))
+  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES | BSR_FLAG_SDMA_COPIES))
     return fail_with(BSR_E_ARG, "unknown config flags 0x%x", config->flags);
   // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
   // each request's ring holds its whole plan and no slot is reused.
   const uint32_t W = config->window_chunks;
   uint32_t b = config->install_batch;
-  // automatic: W - W/8 chunks per launch: large launches, and W/8
-  // chunk-copies of slack before a slot's next copy needs its install.  Up
-  // to W = 8 a launch takes the whole window (the slack would be one chunk,
-  // and measured at W = 8 the larger launch is faster: 52.7 against 52.1
-  // GB/s end to end, four alternating runs each)
+  // automatic: W - max(1, W/8) chunks per launch: large launches, and at
+  // least one chunk-copy of slack before a slot's next copy needs its
+  // install (W = 1 has no slack to give).  A whole-window launch makes the
+  // first copy of every window wait for the previous window's install: at
+  // W = 8 (512K 4-group workload, kernel staging copies) b = 8 restores
+  // 55.4 GB/s, b = 4/6/7 56.3; at W = 16, b = 16 55.9, b = 8/12/14 56.7-56.8;
+  // at W = 32, b = 32 56.0, b = 24/28 57.0.
   if (b == 0)
     b = W == 0 ? static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)
-               : std::max(1u, std::min(W <= 8 ? W : W - W / 8, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
+               : std::max(1u, std::min(W - std::max(1u, W / 8), static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH)));
   if ((W && b > W) || b > BSR_MAX_INSTALL_BATCH)
     return fail_with(BSR_E_ARG, "install_batch %u must be <= min(W=%u, %d)", b, W, BSR_MAX_INSTALL_BATCH);
   // admission (§3 "Install locally": one bounded restore at a time; §7: a
@@ -684,6 +708,7 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
                      b, wpc);
   }
   c->cfg = *config;
+  c->kernel_copies = (config->flags & BSR_FLAG_SDMA_COPIES) == 0;
   c->W = W;
   c->batch = b;
   c->device = config->hip_device;
@@ -845,14 +870,40 @@ int bsr_store_reserve(bsr_ctx* c, uint64_t bytes) {
   void* p = nullptr;
   if (hipHostMalloc(&p, bytes ? bytes : 1, hipHostMallocDefault) != hipSuccess || !p)
     return fail_with(BSR_E_NOMEM, "hipHostMalloc(%llu) failed", (unsigned long long)bytes);
-  return store_init(c, static_cast<uint8_t*>(p), bytes, true);
+  store_init(c, static_cast<uint8_t*>(p), bytes, true);
+  void* dv = nullptr;
+  if (hipHostGetDevicePointer(&dv, p, 0) == hipSuccess)
+    c->store.arena_dev = static_cast<const uint8_t*>(dv);
+  else
+    (void)hipGetLastError();
+  return BSR_OK;
+}
+
+// The device's view of a caller's arena, if HIP reports both its first and
+// its last byte as pinned host memory mapped contiguously for the device;
+// null otherwise (the copy engine then copies out of it).
+static const uint8_t* pinned_device_view(const void* arena, uint64_t bytes) {
+  if (!bytes) return nullptr;
+  hipPointerAttribute_t a{}, b{};
+  const uint8_t* last = static_cast<const uint8_t*>(arena) + (bytes - 1);
+  if (hipPointerGetAttributes(&a, arena) != hipSuccess || hipPointerGetAttributes(&b, last) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  if (a.type != hipMemoryTypeHost || b.type != hipMemoryTypeHost || !a.devicePointer || !b.devicePointer)
+    return nullptr;
+  const uint8_t* d0 = static_cast<const uint8_t*>(a.devicePointer);
+  if (static_cast<const uint8_t*>(b.devicePointer) != d0 + (bytes - 1)) return nullptr;
+  return d0;
 }
 
 int bsr_store_adopt(bsr_ctx* c, void* host_arena, uint64_t bytes) {
   if (!c || !host_arena) return fail_with(BSR_E_ARG, "ctx or arena is NULL");
   std::lock_guard<std::mutex> lk(c->mu);
   if (c->store.arena) return fail_with(BSR_E_STATE, "store arena already set");
-  return store_init(c, static_cast<uint8_t*>(host_arena), bytes, false);
+  store_init(c, static_cast<uint8_t*>(host_arena), bytes, false);
+  if (c->device >= 0 && set_device(c) == BSR_OK) c->store.arena_dev = pinned_device_view(host_arena, bytes);
+  return BSR_OK;
 }
 
 static void drop_entry(bsr_ctx* c, uint32_t g, uint64_t key) {
@@ -1316,9 +1367,9 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   const uint64_t deadline = c->cfg.window_timeout_ms ? t_window + static_cast<uint64_t>(c->cfg.window_timeout_ms) * 1000000ull : 0;
 
   // Consecutive chunks whose pinned sources are adjacent in the arena and
-  // whose slots are adjacent in the ring are copied by one hipMemcpyAsync:
-  // every copy pays a fixed start-up cost on the copy engine that a 16 MB
-  // chunk does not amortise.  A run waits once, for the release its first
+  // whose slots are adjacent in the ring are staged by one copy: every copy
+  // pays a fixed start-up cost (a kernel launch, or the copy engine's own)
+  // that a 16 MB chunk does not amortise.  A run waits once, for the release its first
   // chunk needs; a chunk needing a later release starts a new run, so no
   // copy waits longer than it would alone.  A run is always issued before
   // the batch holding its chunks is flushed, so the batch's copy event
@@ -1338,7 +1389,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       if (e != hipSuccess) return e;
       s.copy_waited_seq = run.need;
     }
-    e = hipMemcpyAsync(run.dst, run.src, run.bytes, hipMemcpyHostToDevice, s.copy);
+    e = stage_copy(c, s, run.dst, run.src, run.bytes, c->store.arena, c->store.arena_dev, c->store.arena_bytes);
     if (e == hipSuccess) run = Run{};
     return e;
   };
@@ -1353,7 +1404,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     }
     run = Run{};
     if (int r2 = flush_batch(c, s)) return launch_failed(c, s, r2);
-    fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", first, why.c_str());
+    fail_with(BSR_E_TRANSFER, "chunk %u: staging copy failed: %s", first, why.c_str());
     return host_fail(c, s, BSR_FAIL_TRANSFER, first, all_mask, BSR_E_TRANSFER);
   };
   // install what is staged so far: the pending run's copy first
@@ -1461,12 +1512,16 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
           return launch_failed(c, s, rc);
         s.copy_waited_seq = need_seq;
       }
-      if (src_block) {
-        e = hipMemcpyAsync(dst, src_block, c->geo.slot_bytes, hipMemcpyHostToDevice, s.copy);
+      if (src_block && from_file) {
+        e = stage_copy(c, s, dst, src_block, c->geo.slot_bytes, c->ftier.bounce_base(bounce),
+                       c->ftier.bounce_device(bounce), c->ftier.file_bytes());
+      } else if (src_block) {
+        e = stage_copy(c, s, dst, src_block, c->geo.slot_bytes, c->store.arena, c->store.arena_dev,
+                       c->store.arena_bytes);
       } else {
         for (uint32_t g = 0; g < G && e == hipSuccess; ++g)
-          e = hipMemcpyAsync(dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
-                             c->geo.payload[g], hipMemcpyHostToDevice, s.copy);
+          e = stage_copy(c, s, dst + c->geo.offset[g], c->store.block_ptr(ent[g].block) + c->geo.offset[g],
+                         c->geo.payload[g], c->store.arena, c->store.arena_dev, c->store.arena_bytes);
       }
       if (e == hipSuccess && from_file) {
         // the bounce buffer is free again once this copy has run
@@ -1481,7 +1536,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       if (e != hipSuccess) {
         const std::string why = hipGetErrorString(e);
         if ((rc = flush_batch(c, s))) return launch_failed(c, s, rc);
-        fail_with(BSR_E_TRANSFER, "chunk %u: hipMemcpyAsync failed: %s", i, why.c_str());
+        fail_with(BSR_E_TRANSFER, "chunk %u: staging copy failed: %s", i, why.c_str());
         return host_fail(c, s, BSR_FAIL_TRANSFER, i, all_mask, BSR_E_TRANSFER);
       }
     }
@@ -1754,6 +1809,43 @@ int bsr_debug_inject(bsr_ctx* c, int32_t kind, uint32_t chunk, uint32_t param) {
   std::lock_guard<std::mutex> lk(c->mu);
   c->inject = Inject{kind, chunk, param};
   return BSR_OK;
+}
+
+int bsr_measure_stage(bsr_ctx* c, uint64_t bytes, uint32_t reps, double* gbps) {
+  if (!c || !gbps || bytes == 0 || reps == 0 || bytes % 16) return fail_with(BSR_E_ARG, "bad arguments");
+  if (int rc = set_device(c)) return rc;
+  void* h = nullptr;
+  void* d = nullptr;
+  void* hd = nullptr;
+  hipStream_t st = nullptr;
+  hipEvent_t ev[2] = {};
+  int rc = BSR_OK;
+  if (hipHostMalloc(&h, bytes, hipHostMallocDefault) != hipSuccess || hipMalloc(&d, bytes) != hipSuccess ||
+      hipHostGetDevicePointer(&hd, h, 0) != hipSuccess)
+    rc = fail_with(BSR_E_NOMEM, "buffers for the staging-copy measurement");
+  if (!rc) rc = hip_check(hipStreamCreate(&st), "hipStreamCreate");
+  for (int i = 0; !rc && i < 2; ++i) rc = hip_check(hipEventCreate(&ev[i]), "hipEventCreate");
+  if (!rc) {
+    std::memset(h, 0x5a, bytes);
+    double best = 0;
+    for (uint32_t r = 0; r < reps && !rc; ++r) {
+      rc = hip_check(hipEventRecord(ev[0], st), "hipEventRecord");
+      if (!rc) rc = hip_check(bsr::launch_stage(bsr::StageParams{static_cast<const uint8_t*>(hd), static_cast<uint8_t*>(d), bytes}, st), "staging copy");
+      if (!rc) rc = hip_check(hipEventRecord(ev[1], st), "hipEventRecord");
+      if (!rc) rc = hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
+      float ms = 0;
+      if (!rc) rc = hip_check(hipEventElapsedTime(&ms, ev[0], ev[1]), "hipEventElapsedTime");
+      if (!rc && ms > 0) best = std::max(best, bytes / (ms * 1e-3) / 1e9);
+    }
+    *gbps = best;
+  }
+  if (st) (void)hipStreamSynchronize(st);
+  for (auto e : ev)
+    if (e) (void)hipEventDestroy(e);
+  if (st) (void)hipStreamDestroy(st);
+  if (d) (void)hipFree(d);
+  if (h) (void)hipHostFree(h);
+  return rc;
 }
 
 int bsr_measure_h2d(bsr_ctx* c, uint64_t bytes, uint32_t n_streams, uint32_t reps, double* gbps) {

@@ -107,11 +107,14 @@ def measured_restore(gc: GpuCase, request_id: int, n_hit: int, **kw):
 
     The ring is dropped and allocated again by the bind, inside the measured
     region, after the pools and the status block.  Returns the outcome and
-    {"peak_alloc_delta": growth of torch's peak allocated bytes from before
-    the ring to after the commit, "free_after_bind" / "free_after_commit":
+    {"peak_requested_delta": growth of torch's peak requested bytes from
+    before the ring to after the commit, "peak_alloc_delta": the same in
+    allocated bytes (block sizes, which torch may round up: it keeps a
+    segment's remainder of at most 1 MiB unsplit), "free_after_bind" /
+    "free_after_commit":
     the device's free bytes (hipMemGetInfo)}: a restore that allocates
-    nothing but its ring grows the peak by exactly the ring and leaves the
-    free bytes unchanged from bind to commit.
+    nothing but its ring grows the requested peak by exactly the ring and
+    leaves the free bytes unchanged from bind to commit.
 
     The first restores of a process see the HIP runtime set up its queues
     for the session's streams and grow its internal pools with the depth of
@@ -130,6 +133,7 @@ def measured_restore(gc: GpuCase, request_id: int, n_hit: int, **kw):
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
+    base_req = torch.cuda.memory_stats()["requested_bytes.all.current"]
     m = {}
 
     def after_bind():
@@ -137,4 +141,5 @@ def measured_restore(gc: GpuCase, request_id: int, n_hit: int, **kw):
     out = gc.restore(request_id, n_hit, after_bind=after_bind, **kw)
     m["free_after_commit"] = torch.cuda.mem_get_info()[0]
     m["peak_alloc_delta"] = torch.cuda.max_memory_allocated() - base
+    m["peak_requested_delta"] = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base_req
     return out, m

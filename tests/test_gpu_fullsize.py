@@ -79,7 +79,8 @@ def _check_valid(gc, wi, expected):
 
 def _check_staging_measured(m, W, slot_bytes):
     """Eq. 1 across the restore: the ring is the only device memory it adds."""
-    assert m["peak_alloc_delta"] == W * slot_bytes, m
+    assert m["peak_requested_delta"] == W * slot_bytes, m
+    assert 0 <= m["peak_alloc_delta"] - W * slot_bytes <= 1 << 20, m   # torch's block rounding
     assert m["free_after_commit"] == m["free_after_bind"], m
 
 

@@ -113,8 +113,9 @@ def test_capacity_contrast_128k():
             assert out.exposed_tokens == 98_304 and out.fallback == 0
             peaks[W] = out.stats["peak_live_staging_bytes"]
             ring = (W or n) * layout.slot_bytes
+            assert m["peak_requested_delta"] == ring, m
             # torch may keep a remainder of at most 1 MiB unsplit in the ring's segment
-            assert 0 <= m["peak_alloc_delta"] - ring <= (1 << 20 if W == 0 else 0), m
+            assert 0 <= m["peak_alloc_delta"] - ring <= 1 << 20, m
             assert m["free_after_commit"] == m["free_after_bind"], m
             valid = [v.copy() for v in wi.valid_init]
             oracle.set_request_valid(layout, n, wi.block_tables, valid, 1)
