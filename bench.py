@@ -23,6 +23,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+# MI355X's host interface, PCIe Gen5 x16, per direction: 32 GT/s x 16 lanes
+# x 128/130 encoding / 8 bits
+LINK_PEAK_GBPS = 32 * 16 * 128 / 130 / 8
 
 
 def log(*a):
@@ -187,6 +190,9 @@ def main():
     avg_launch_ms = kern_ms / launches
     bytes_per_launch = 2 * installed / launches        # read staged + write paged
     achieved = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
+    stage_launches = sum(o[1].stats["n_stage_launches"] for o in outs)
+    stage_ms = sum(o[1].stats["stage_ms_total"] for o in outs)
+    stage_bytes = sum(o[1].stats["stage_bytes"] for o in outs)
     st = outs[-1][1].stats
 
     if args.calibrate_copy:
@@ -265,6 +271,16 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "traffic_source": traffic_src,
             "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(avg_launch_ms * 1e3, 2),
             "launches_timed": launches,
+        },
+        "roofline_stage": None if not stage_launches else {
+            "bound": "host link", "kernel": "k_stage",
+            "achieved": round(stage_bytes / (stage_ms * 1e-3) / 1e9, 3), "peak": round(LINK_PEAK_GBPS, 3),
+            "unit": "GB/s", "frac": round(stage_bytes / (stage_ms * 1e-3) / 1e9 / LINK_PEAK_GBPS, 4),
+            "frac_of_measured_link": round(stage_bytes / (stage_ms * 1e-3) / 1e9 / h2d, 4),
+            "bytes_per_launch": int(stage_bytes / stage_launches),
+            "avg_launch_us": round(stage_ms / stage_launches * 1e3, 2), "launches_timed": stage_launches,
+            "note": "bytes read over the host link (pinned host memory -> ring) per ms of the staging kernel, "
+                    "HIP events on the copy stream; peak = PCIe Gen5 x16 per direction after encoding",
         },
         "hbm_copy_context": {
             "achieved": round(copy_gbps, 1), "unit": "GB/s", "frac": round(copy_gbps / HBM_PEAK_GBPS, 4),

@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define BSR_ABI_VERSION 2
+#define BSR_ABI_VERSION 3
 #define BSR_MAX_GROUPS 8
 #define BSR_MAX_INSTALL_BATCH 32
 #define BSR_MAX_BOUND_REQUESTS 16 /* session slots of one context */
@@ -97,7 +97,7 @@ extern "C" {
 #define BSR_KIND_PLANAR 1
 
 /* bsr_config.flags */
-#define BSR_FLAG_TIME_INSTALL 1u  /* time every install launch with HIP events */
+#define BSR_FLAG_TIME_INSTALL 1u  /* time every install and staging-copy launch with HIP events */
 #define BSR_FLAG_TRUSTED_TABLES 2u /* bind does not read the block tables back, so it never waits for the
                                       compute stream (an engine's model work may be queued there); the
                                       tables are checked on the device after the begin kernel instead: an
@@ -226,7 +226,9 @@ typedef struct bsr_stats {
   double install_ms_max;           /* longest install launch (BSR_FLAG_TIME_INSTALL) */
   uint64_t host_bounce_bytes;      /* pinned host landing zone of the file tier (when it served chunks) */
   uint32_t file_tier_chunks;       /* chunks restored from the file tier */
-  uint32_t reserved0;
+  uint32_t n_stage_launches;       /* staging-copy kernel launches (0 when the copy engine staged) */
+  uint64_t stage_bytes;            /* bytes those launches moved from pinned host memory */
+  double stage_ms_total;           /* sum of their durations (BSR_FLAG_TIME_INSTALL) */
 } bsr_stats;
 
 /* Admission state of a context (the lock or the global budget B). */

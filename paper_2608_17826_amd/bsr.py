@@ -18,7 +18,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbsr.so")
 
-BSR_ABI_VERSION = 2
+BSR_ABI_VERSION = 3
 BSR_MAX_GROUPS = 8
 BSR_MAX_INSTALL_BATCH = 32
 BSR_MAX_BOUND_REQUESTS = 16
@@ -82,7 +82,8 @@ class bsr_stats(ct.Structure):
                 ("probe_ns", ct.c_uint64), ("enqueue_ns", ct.c_uint64), ("commit_wait_ns", ct.c_uint64),
                 ("install_ms_total", ct.c_double), ("install_ms_max", ct.c_double),
                 ("host_bounce_bytes", ct.c_uint64), ("file_tier_chunks", ct.c_uint32),
-                ("reserved0", ct.c_uint32)]
+                ("n_stage_launches", ct.c_uint32), ("stage_bytes", ct.c_uint64),
+                ("stage_ms_total", ct.c_double)]
 
 
 class bsr_admission(ct.Structure):

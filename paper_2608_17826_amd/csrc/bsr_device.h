@@ -305,7 +305,7 @@ void static_scratch_release(int device);
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s,
                           hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_verify(const VerifyParams& p, hipStream_t s);
-hipError_t launch_stage(const StageParams& p, hipStream_t s);
+hipError_t launch_stage(const StageParams& p, hipStream_t s, hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_finish(const FinishParams& p, hipStream_t s);
 
 }  // namespace bsr

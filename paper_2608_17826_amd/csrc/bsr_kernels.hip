@@ -1,5 +1,9 @@
 // gfx950 kernels of the bounded-window restore.
 //
+// stage   : copy a run of staged chunks from pinned host memory into the
+//           W-slot ring (§4 windowed retrieve: the window's objects are
+//           brought into the local restore pool), read over the host link
+//           by a small grid on the copy stream.
 // install : scatter staged chunks from the W-slot ring into every group's
 //           paged blocks (§3 "Install locally"; §4 windowed retrieve, whose
 //           per-window step moves the staged window into the engine's
@@ -22,8 +26,9 @@
 //           (Eq. 6), invalidate (§4 failed-block + HMA-aware invalidation),
 //           mark one group invalid, check the block tables on the device.
 //
-// Nothing here is a dense contraction: the path is bound by HBM bandwidth
-// (read the staged chunk once, write the paged blocks once).
+// Nothing here is a dense contraction.  The staging copy is bound by the
+// host link; the install by HBM bandwidth (read the staged chunk once,
+// write the paged blocks once).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -734,13 +739,16 @@ hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_stage(const StageParams& p, hipStream_t s) {
+hipError_t launch_stage(const StageParams& p, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
   if (((reinterpret_cast<uintptr_t>(p.src) | reinterpret_cast<uintptr_t>(p.dst)) & 15u) || (p.bytes & 3u))
     return hipErrorInvalidValue;
   if (p.bytes == 0) return hipSuccess;
   const uint64_t per_wg = static_cast<uint64_t>(kStageThreads) * kStageUnroll * 16;
-  const uint64_t grid = std::min<uint64_t>(kStageMaxGrid, (p.bytes + per_wg - 1) / per_wg);
-  hipLaunchKernelGGL(k_stage, dim3(static_cast<uint32_t>(grid)), dim3(kStageThreads), 0, s, p);
+  const uint32_t grid = static_cast<uint32_t>(std::min<uint64_t>(kStageMaxGrid, (p.bytes + per_wg - 1) / per_wg));
+  if (start && stop)
+    hipExtLaunchKernelGGL(k_stage, dim3(grid), dim3(kStageThreads), 0, s, start, stop, 0, p);
+  else
+    hipLaunchKernelGGL(k_stage, dim3(grid), dim3(kStageThreads), 0, s, p);
   return hipGetLastError();
 }
 

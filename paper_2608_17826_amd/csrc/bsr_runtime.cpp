@@ -371,7 +371,8 @@ struct Session {  // one bound request
   int64_t batch_seq = 0;
   uint32_t slots_touched = 0;
   std::vector<uint8_t> slot_used;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> timing;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> timing;        // install launches
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> stage_timing;  // staging-copy launches
   // chunks copied but not yet installed (the current install batch)
   std::vector<uint32_t> pend;
   std::vector<std::array<uint64_t, BSR_MAX_GROUPS>> pend_tags;
@@ -471,7 +472,26 @@ hipError_t stage_copy(bsr_ctx* c, Session& s, uint8_t* dst, const uint8_t* src, 
   const bool dst_in = dst >= s.staging && bytes <= s.ring_bytes &&
                       static_cast<uint64_t>(dst - s.staging) <= s.ring_bytes - bytes;
   if (!src_in || !dst_in) return hipErrorInvalidValue;
-  return bsr::launch_stage(bsr::StageParams{dev + (src - base), dst, bytes}, s.copy);
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
+    t0 = take_timing_event(c);
+    t1 = take_timing_event(c);
+    if (!t0 || !t1) {
+      if (t0) c->timing_pool.push_back(t0);
+      if (t1) c->timing_pool.push_back(t1);
+      t0 = t1 = nullptr;
+    }
+  }
+  const hipError_t e = bsr::launch_stage(bsr::StageParams{dev + (src - base), dst, bytes}, s.copy, t0, t1);
+  if (e != hipSuccess) {
+    if (t0) c->timing_pool.push_back(t0);
+    if (t1) c->timing_pool.push_back(t1);
+    return e;
+  }
+  if (t0) s.stage_timing.emplace_back(t0, t1);
+  ++s.st.n_stage_launches;
+  s.st.stage_bytes += bytes;
+  return hipSuccess;
 }
 
 // Enqueue install + verify for the chunks staged since the last flush.
@@ -834,10 +854,11 @@ int bsr_ctx_destroy(bsr_ctx* c) {
       Session& s = kv.second;
       if (s.copy) (void)hipStreamSynchronize(s.copy);
       if (s.compute) (void)hipStreamSynchronize(s.compute);
-      for (auto& pr : s.timing) {
-        (void)hipEventDestroy(pr.first);
-        (void)hipEventDestroy(pr.second);
-      }
+      for (auto* v : {&s.timing, &s.stage_timing})
+        for (auto& pr : *v) {
+          (void)hipEventDestroy(pr.first);
+          (void)hipEventDestroy(pr.second);
+        }
     }
     for (SessionRes& r : c->res) free_session_res(r);
     if (c->static_claimed) bsr::static_scratch_release(c->device);
@@ -1650,6 +1671,15 @@ static int complete_session(bsr_ctx* c, Session& s, std::unique_lock<std::mutex>
   s.timing.clear();
   st.install_ms_total = tot;
   st.install_ms_max = mx;
+  double stot = 0;
+  for (auto& pr : s.stage_timing) {
+    float ms = 0;
+    if (hipEventElapsedTime(&ms, pr.first, pr.second) == hipSuccess) stot += ms;
+    c->timing_pool.push_back(pr.first);
+    c->timing_pool.push_back(pr.second);
+  }
+  s.stage_timing.clear();
+  st.stage_ms_total = stot;
   release_refs(c, s);
   const uint64_t id = s.id;
   auto it = c->requests.find(id);
