@@ -55,6 +55,12 @@ def parse():
                     help="file tier only: comma-separated load concurrencies to measure as well")
     ap.add_argument("--copy-engine", choices=["kernel", "sdma"], default="kernel",
                     help="staging copies by the library's kernel (default) or by the copy engine")
+    ap.add_argument("--only-group", type=int, default=-1,
+                    help="profiling: install one group of the workload alone, its tensor count scaled so that a "
+                         "chunk holds as many bytes as the whole layout's chunk (the same launch size)")
+    ap.add_argument("--scatter-ceiling", action="store_true",
+                    help="also measure a plain scattered copy of each group's block size at the install's "
+                         "launch size (bsr_measure_scatter)")
     ap.add_argument("--requests", type=int, default=1,
                     help="requests bound at once under a global admission budget B = requests x ring "
                          "(each with its own ring and destination pools; windows interleaved)")
@@ -77,6 +83,8 @@ def main():
     from workloads.device import place
 
     w = get_config(args.workload)
+    if args.only_group >= 0:
+        w = group_alone(w, args.only_group)
     W = args.window
     log(f"[bench] workload {w.index} {w.name}: generating inputs")
     wi = generate(w)
@@ -235,6 +243,22 @@ def main():
 
     staging_measured = measure_staging(torch, bsr, ctx, sess, wi, dsts, 9000) if K == 1 else None
 
+    ceiling = None
+    if args.scatter_ceiling:
+        # the install's data per full launch, copied as plain scattered blocks of each group's size
+        data = st["install_batch"] * chunk_payload
+        ceiling = {"data_bytes_per_launch": data,
+                   "note": "bsr_measure_scatter: best of 5, read + write bytes; the source read cold, or rewritten "
+                           "right before each launch as the staging copy writes a slot before the install"}
+        for spec in w.groups:
+            bb = spec.block_tokens * spec.record_bytes
+            if bb % 16 == 0 and str(bb) not in ceiling:
+                cold = bsr.bsr_measure_scatter(ctx, bb, data, 5, 1)
+                warm = bsr.bsr_measure_scatter(ctx, bb, data, 5, 1, bsr.BSR_SCATTER_WARM_SOURCE)
+                ceiling[str(bb)] = {"cold_source_gbps": round(cold, 1), "cold_source_frac": round(cold / HBM_PEAK_GBPS, 4),
+                                    "warm_source_gbps": round(warm, 1), "warm_source_frac": round(warm / HBM_PEAK_GBPS, 4)}
+                log(f"[bench] scatter ceiling, {bb} B blocks: {cold:.1f} GB/s cold source, {warm:.1f} warm")
+
     cpu = None
     if not args.no_cpu_baseline and W > 0 and K == 1:
         cpu = cpu_baseline(wi, W, args.cpu_seconds)
@@ -282,6 +306,7 @@ def main():
             "note": "bytes read over the host link (pinned host memory -> ring) per ms of the staging kernel, "
                     "HIP events on the copy stream; peak = PCIe Gen5 x16 per direction after encoding",
         },
+        "scatter_ceiling": ceiling,
         "hbm_copy_context": {
             "achieved": round(copy_gbps, 1), "unit": "GB/s", "frac": round(copy_gbps / HBM_PEAK_GBPS, 4),
             "measured_as": "torch copy_ of 1 GiB device to device (read + write bytes), best of 5",
@@ -323,6 +348,21 @@ def main():
                              "concurrency_sweep": sweep}
     print(json.dumps(line), flush=True)
     bsr.bsr_ctx_destroy(ctx)
+
+
+def group_alone(w, g):
+    """Workload w with only group g, its tensor count scaled so that a chunk
+    holds about as many bytes as the whole layout's chunk: install launches of
+    the same size as the layout's, built from that group's blocks alone."""
+    import dataclasses
+
+    spec = w.groups[g]
+    per_token = sum(s.n_tensors * s.record_bytes for s in w.groups)
+    nt = max(1, round(per_token / spec.record_bytes))
+    base = max(w.base_records or 0, nt * w.chunk_tokens + w.held_chunks)
+    return dataclasses.replace(w, name=f"{w.name}-{spec.name}-alone",
+                               groups=(dataclasses.replace(spec, n_tensors=nt),), base_records=base,
+                               failure=None, failure_group=None)
 
 
 def measure_staging(torch, bsr, ctx, sess, wi, dsts, rid):

@@ -523,6 +523,20 @@ int bsr_measure_h2d(bsr_ctx* ctx, uint64_t bytes, uint32_t n_streams, uint32_t r
  * context. */
 int bsr_measure_stage(bsr_ctx* ctx, uint64_t bytes, uint32_t reps, double* gbps);
 
+/* A ceiling for the install kernel: a plain copy of data_bytes / block_bytes
+ * whole blocks from a contiguous device buffer into as many distinct blocks
+ * of a pool twice the data, drawn in a seeded random order, with the
+ * install's workgroup shape, occupancy and XCD work order, and nothing else
+ * (no tag, no metadata, no status check).  With BSR_SCATTER_WARM_SOURCE the
+ * source is rewritten (a device fill) right before every timed launch, as
+ * the staging copy writes a ring slot right before the install reads it;
+ * otherwise it is read cold.  Best of `reps` launches; *gbps counts read +
+ * write bytes (1e9 B/s).  block_bytes: a positive multiple of 16.  Allocates
+ * its own buffers.  Needs a GPU context. */
+#define BSR_SCATTER_WARM_SOURCE 1u
+int bsr_measure_scatter(bsr_ctx* ctx, uint32_t block_bytes, uint64_t data_bytes, uint32_t reps,
+                        uint64_t seed, uint32_t flags, double* gbps);
+
 #ifdef __cplusplus
 }
 #endif

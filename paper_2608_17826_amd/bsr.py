@@ -136,6 +136,7 @@ def _load() -> ct.CDLL:
         "bsr_debug_inject": (ct.c_int, [VP, I32, U32, U32]),
         "bsr_measure_h2d": (ct.c_int, [VP, U64, U32, U32, P(ct.c_double)]),
         "bsr_measure_stage": (ct.c_int, [VP, U64, U32, P(ct.c_double)]),
+        "bsr_measure_scatter": (ct.c_int, [VP, U32, U64, U32, U64, U32, P(ct.c_double)]),
         "bsr_file_tier_open": (ct.c_int, [VP, ct.c_char_p, U32, U32, U32]),
         "bsr_file_tier_put_chunk": (ct.c_int, [VP, U64, P(VP)]),
         "bsr_file_tier_remove": (ct.c_int, [VP, U64, I32]),
@@ -373,6 +374,16 @@ def bsr_debug_inject(ctx: Ctx, kind: int, chunk: int = 0, param: int = 0) -> Non
 def bsr_measure_h2d(ctx: Ctx, nbytes: int, n_streams: int = 1, reps: int = 10) -> float:
     g = ct.c_double()
     _check(_lib.bsr_measure_h2d(ctx, nbytes, n_streams, reps, ct.byref(g)))
+    return g.value
+
+
+BSR_SCATTER_WARM_SOURCE = 1
+
+
+def bsr_measure_scatter(ctx: Ctx, block_bytes: int, data_bytes: int, reps: int = 5, seed: int = 1,
+                        flags: int = 0) -> float:
+    g = ct.c_double()
+    _check(_lib.bsr_measure_scatter(ctx, block_bytes, data_bytes, reps, seed, flags, ct.byref(g)))
     return g.value
 
 

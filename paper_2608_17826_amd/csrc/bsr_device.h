@@ -274,15 +274,17 @@ struct StageParams {
   uint64_t bytes;
 };
 // Shape: the host link needs about its bandwidth-delay product in flight,
-// and reads queued beyond it delay the install's HBM traffic.  32
-// workgroups x 256 threads x 2 vectors keep 256 KiB in flight: 57.6 GB/s
-// from pinned memory, and installs that overlap the copy run as fast as
-// alone (154 us per 28-chunk launch at the 512K 4-group workload).  Measured
-// in the restore (grid x vectors: link GB/s, W = 32 install us): 64 x 4
-// (1 MiB in flight) 57.5, 468; 32 x 4: 56.9, 200; 24 x 4: 55.5, 173;
-// 64 x 1: 57.6, 161; 16 x 4: 57.2, 156; 8 x 8: 57.3, 150.
+// and reads queued beyond it delay the install's HBM traffic when the two
+// overlap.  24 workgroups x 256 threads x 2 vectors keep 192 KiB in flight.
+// Measured on one box, 512K 4-group workload (grid x vectors, KiB in
+// flight: restore GB/s at W = 32, install's share of 8 TB/s at W = 32 and
+// W = 8): 24 x 2, 192: 56.84, 76.5%, 62.9%; 32 x 2, 256: 56.87, 74.3%,
+// 55.8%; 48 x 1, 192: 56.61, 75.1% (W = 32 only); 16 x 2 and 32 x 1, 128:
+// 56.44-56.59, 79.1%, 72.4%; 64 x 4, 1 MiB: installs three times slower.
+// Staging that keeps less in flight moves less over the link (8 x 4, 128:
+// 55.9 GB/s of link), so 192 KiB is the shape that keeps the link's rate.
 #ifndef BSR_STAGE_GRID
-#define BSR_STAGE_GRID 32
+#define BSR_STAGE_GRID 24
 #endif
 #ifndef BSR_STAGE_UNROLL
 #define BSR_STAGE_UNROLL 2
@@ -301,6 +303,24 @@ constexpr uint64_t kStaticScratchBytes = BSR_STATIC_SCRATCH_BYTES;
 constexpr int kMaxScratchDevices = 64;
 hipError_t static_scratch_claim(int device, void** ptr, bool* busy);
 void static_scratch_release(int device);
+
+// Ceiling for the install (bsr_measure_scatter): a plain copy of whole
+// blocks from a contiguous source into scattered destination blocks, with
+// the install's workgroup shape, occupancy (lds_bytes) and XCD work order,
+// and nothing else.
+struct ScatterParams {
+  const uint8_t* src;        // n_blocks x block_bytes, contiguous
+  uint8_t* pool;             // destination pool of block_bytes blocks
+  const int32_t* dst_block;  // destination block of each source block
+  uint32_t block_bytes;      // a multiple of 16
+  uint32_t piece_bytes;      // a multiple of kPieceAlign, at most kMaxPieceBytes
+  uint32_t pieces_per_block;
+  uint32_t n_blocks;
+  uint32_t xcd_log2;
+  uint32_t xcd_full;
+  uint32_t lds_bytes;
+};
+hipError_t launch_scatter(const ScatterParams& p, hipStream_t s);
 
 hipError_t launch_install(const InstallParams& p, uint32_t n_workgroups, hipStream_t s,
                           hipEvent_t start = nullptr, hipEvent_t stop = nullptr);

@@ -688,6 +688,51 @@ __global__ __launch_bounds__(kStageThreads) void k_stage(const StageParams p) {
         *global_ptr(reinterpret_cast<const uint32_t*>(p.src) + w0 + threadIdx.x);
 }
 
+// Plain scattered block copy (the install's ceiling, see ScatterParams):
+// one workgroup per piece of a block, every thread four 16-byte vectors.
+// The piece's data loads and the destination block id share one memory
+// round trip (the install's load burst), and the stores are the install's
+// (non-temporal, device scope, through a buffer resource).
+__global__ __launch_bounds__(kInstallThreads) void k_scatter(const ScatterParams p) {
+  const uint32_t tid = threadIdx.x;
+  const uint32_t w = xcd_work_index(blockIdx.x, p.xcd_full, p.xcd_log2);
+  const uint32_t blk = w / p.pieces_per_block, piece = w - blk * p.pieces_per_block;
+  if (blk >= p.n_blocks) return;
+  const uint32_t off = piece * p.piece_bytes;
+  const uint32_t len = (p.block_bytes - off) < p.piece_bytes ? (p.block_bytes - off) : p.piece_bytes;
+  const u32x4* s4 = reinterpret_cast<const u32x4*>(p.src + static_cast<uint64_t>(blk) * p.block_bytes + off);
+  const uint32_t nvec = len >> 4;  // >= 1: len is a positive multiple of 16
+  constexpr uint32_t U = BSR_UNROLL;
+  const u32x4* at[U];
+#pragma unroll
+  for (uint32_t u = 0; u < U; ++u) {
+    const uint32_t i = u * kInstallThreads + tid;
+    at[u] = s4 + (i < nvec - 1 ? i : nvec - 1);
+  }
+  u32x4 v[U];
+  uint32_t mw;
+  LoadBurst<U>::run(v, mw, at, reinterpret_cast<const uint32_t*>(p.dst_block + blk));
+  const int32_t b = static_cast<int32_t>(row_lane(mw, 0));
+  uint8_t* dst = p.pool + static_cast<uint64_t>(b) * p.block_bytes + off;
+  const __amdgpu_buffer_rsrc_t rs = piece_rsrc(dst, len);
+#pragma unroll
+  for (uint32_t u = 0; u < U; ++u) {
+    const uint32_t i = u * kInstallThreads + tid;
+    if (i < nvec) st_piece16(v[u], rs, i * 16u);
+  }
+}
+
+hipError_t launch_scatter(const ScatterParams& p, hipStream_t s) {
+  if (p.xcd_log2 > 5 || p.pieces_per_block == 0 || p.piece_bytes > kMaxPieceBytes || p.piece_bytes % kPieceAlign ||
+      p.block_bytes % 16 || static_cast<uint64_t>(p.pieces_per_block) * p.piece_bytes < p.block_bytes)
+    return hipErrorInvalidValue;
+  const uint64_t grid = static_cast<uint64_t>(p.n_blocks) * p.pieces_per_block;
+  if (grid == 0 || grid >= (1ull << 31) || p.xcd_full != xcd_remap_bound(static_cast<uint32_t>(grid), p.xcd_log2))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_scatter, dim3(static_cast<uint32_t>(grid)), dim3(kInstallThreads), p.lds_bytes, s, p);
+  return hipGetLastError();
+}
+
 // The static scratch.  In host code `scratch` names a host-side stand-in,
 // not device memory: only the address from hipGetSymbolAddress, taken per
 // device with that device current, is ever passed to a kernel or a copy.

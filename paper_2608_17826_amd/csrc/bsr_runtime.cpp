@@ -1841,6 +1841,71 @@ int bsr_debug_inject(bsr_ctx* c, int32_t kind, uint32_t chunk, uint32_t param) {
   return BSR_OK;
 }
 
+int bsr_measure_scatter(bsr_ctx* c, uint32_t block_bytes, uint64_t data_bytes, uint32_t reps, uint64_t seed,
+                        uint32_t flags, double* gbps) {
+  if (flags & ~BSR_SCATTER_WARM_SOURCE) return fail_with(BSR_E_ARG, "unknown flags 0x%x", flags);
+  if (!c || !gbps || reps == 0 || block_bytes == 0 || block_bytes % 16 || data_bytes < block_bytes)
+    return fail_with(BSR_E_ARG, "bad arguments (block_bytes a positive multiple of 16, data_bytes >= block_bytes)");
+  if (int rc = set_device(c)) return rc;
+  const uint64_t nb = data_bytes / block_bytes;
+  const uint64_t n_pieces = (block_bytes + bsr::kMaxPieceBytes - 1) / bsr::kMaxPieceBytes;
+  const uint32_t piece = static_cast<uint32_t>(align_up((block_bytes + n_pieces - 1) / n_pieces, bsr::kPieceAlign));
+  const uint32_t ppb = (block_bytes + piece - 1) / piece;
+  if (nb * ppb >= (1ull << 31) || nb >= (1ull << 30)) return fail_with(BSR_E_ARG, "too many blocks for one launch");
+  // destinations: nb distinct blocks of a pool twice the data, in a seeded random order
+  std::vector<int32_t> perm(2 * nb);
+  for (uint64_t i = 0; i < perm.size(); ++i) perm[i] = static_cast<int32_t>(i);
+  uint64_t x = seed * 0x9E3779B97F4A7C15ull + 1;
+  for (uint64_t i = perm.size() - 1; i > 0; --i) {  // Fisher-Yates with a splitmix64 stream
+    x += 0x9E3779B97F4A7C15ull;
+    uint64_t z = x;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    std::swap(perm[i], perm[z % (i + 1)]);
+  }
+  void* src = nullptr;
+  void* pool = nullptr;
+  void* dperm = nullptr;
+  hipStream_t st = nullptr;
+  hipEvent_t ev[2] = {};
+  int rc = BSR_OK;
+  if (hipMalloc(&src, nb * block_bytes) != hipSuccess || hipMalloc(&pool, 2 * nb * block_bytes) != hipSuccess ||
+      hipMalloc(&dperm, nb * sizeof(int32_t)) != hipSuccess)
+    rc = fail_with(BSR_E_NOMEM, "buffers for the scatter measurement");
+  if (!rc) rc = hip_check(hipStreamCreate(&st), "hipStreamCreate");
+  for (int i = 0; !rc && i < 2; ++i) rc = hip_check(hipEventCreate(&ev[i]), "hipEventCreate");
+  if (!rc) rc = hip_check(hipMemcpy(dperm, perm.data(), nb * sizeof(int32_t), hipMemcpyHostToDevice), "hipMemcpy");
+  if (!rc) rc = hip_check(hipMemset(src, 0x5a, nb * block_bytes), "hipMemset");
+  bsr::ScatterParams p{static_cast<const uint8_t*>(src), static_cast<uint8_t*>(pool),
+                       static_cast<const int32_t*>(dperm), block_bytes, piece, ppb, static_cast<uint32_t>(nb),
+                       c->xcd_log2, bsr::xcd_remap_bound(static_cast<uint32_t>(nb * ppb), c->xcd_log2), c->geo.lds_bytes};
+  if (!rc) {
+    double best = 0;
+    for (uint32_t r = 0; r < reps && !rc; ++r) {
+      // the staging copy writes a slot right before the install reads it
+      if (flags & BSR_SCATTER_WARM_SOURCE)
+        rc = hip_check(hipMemsetAsync(src, 0x30 + r, nb * block_bytes, st), "hipMemsetAsync");
+      if (!rc) rc = hip_check(hipEventRecord(ev[0], st), "hipEventRecord");
+      if (!rc) rc = hip_check(bsr::launch_scatter(p, st), "scatter launch");
+      if (!rc) rc = hip_check(hipEventRecord(ev[1], st), "hipEventRecord");
+      if (!rc) rc = hip_check(hipEventSynchronize(ev[1]), "hipEventSynchronize");
+      float ms = 0;
+      if (!rc) rc = hip_check(hipEventElapsedTime(&ms, ev[0], ev[1]), "hipEventElapsedTime");
+      if (!rc && ms > 0) best = std::max(best, 2.0 * nb * block_bytes / (ms * 1e-3) / 1e9);
+    }
+    *gbps = best;
+  }
+  if (st) (void)hipStreamSynchronize(st);
+  for (auto e : ev)
+    if (e) (void)hipEventDestroy(e);
+  if (st) (void)hipStreamDestroy(st);
+  if (dperm) (void)hipFree(dperm);
+  if (pool) (void)hipFree(pool);
+  if (src) (void)hipFree(src);
+  return rc;
+}
+
 int bsr_measure_stage(bsr_ctx* c, uint64_t bytes, uint32_t reps, double* gbps) {
   if (!c || !gbps || bytes == 0 || reps == 0 || bytes % 16) return fail_with(BSR_E_ARG, "bad arguments");
   if (int rc = set_device(c)) return rc;

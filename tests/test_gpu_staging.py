@@ -117,3 +117,22 @@ def test_staging_kernel_link_rate_reported():
             bsr.bsr_measure_stage(ctx, 1000, 1)      # not a multiple of 16
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_scatter_ceiling_measurement():
+    """The plain scattered-copy ceiling runs for the layouts' block sizes,
+    cold and warm, and rejects block sizes that are not 16-byte multiples."""
+    wi = generate(get_config(1))
+    ctx = bsr.bsr_ctx_create(layout_of(wi), 2, hip_device=0)
+    try:
+        for bb in (73_728, 16_896, 16_384):
+            cold = bsr.bsr_measure_scatter(ctx, bb, 64 << 20, 2, 1)
+            warm = bsr.bsr_measure_scatter(ctx, bb, 64 << 20, 2, 1, bsr.BSR_SCATTER_WARM_SOURCE)
+            say(f"{bb} B blocks: {cold:.0f} GB/s cold, {warm:.0f} GB/s warm")
+            assert cold > 100 and warm > 100
+        with pytest.raises(bsr.BsrError):
+            bsr.bsr_measure_scatter(ctx, 1000, 64 << 20, 1, 1)
+        with pytest.raises(bsr.BsrError):
+            bsr.bsr_measure_scatter(ctx, 16_384, 64 << 20, 1, 1, 2)     # unknown flag
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
