@@ -55,6 +55,8 @@ def parse():
                     help="file tier only: comma-separated load concurrencies to measure as well")
     ap.add_argument("--copy-engine", choices=["kernel", "sdma"], default="kernel",
                     help="staging copies by the library's kernel (default) or by the copy engine")
+    ap.add_argument("--two-streams", action="store_true",
+                    help="stage on the copy stream whatever the request's size (BSR_FLAG_TWO_STREAMS)")
     ap.add_argument("--only-group", type=int, default=-1,
                     help="profiling: install one group of the workload alone, its tensor count scaled so that a "
                          "chunk holds as many bytes as the whole layout's chunk (the same launch size)")
@@ -98,7 +100,8 @@ def main():
     slot = bsr.bsr_slot_bytes(layout)
     held_plan = w.held_chunks if not args.held_chunks else min(args.held_chunks, w.held_chunks)
     budget = 0 if K == 1 else K * (W or held_plan) * slot
-    copy_flag = bsr.BSR_FLAG_SDMA_COPIES if args.copy_engine == "sdma" else 0
+    copy_flag = (bsr.BSR_FLAG_SDMA_COPIES if args.copy_engine == "sdma" else 0) | \
+        (bsr.BSR_FLAG_TWO_STREAMS if args.two_streams else 0)
     ctx = bsr.bsr_ctx_create(layout, W, hip_device=0, install_batch=args.install_batch,
                              flags=bsr.BSR_FLAG_TIME_INSTALL | copy_flag, staging_budget_bytes=budget,
                              max_bound_requests=0 if K == 1 else K)

@@ -104,6 +104,10 @@ extern "C" {
                                       id outside [0, pool_blocks) fails the request (fail = BSR_FAIL_BLOCK_TABLE,
                                       nothing exposed; the kernels never write such an id).  The caller
                                       guarantees that no id repeats within one group's prefix (not checked) */
+#define BSR_FLAG_TWO_STREAMS 8u   /* stage every request on the copy stream.  By default a request of at
+                                      most 64 MiB of chunks is staged on the compute stream, so that stream
+                                      order, not events between the two streams, orders its copies,
+                                      installs and slot reuse */
 #define BSR_FLAG_SDMA_COPIES 4u   /* stage chunks with the copy engine (hipMemcpyAsync) instead of the
                                       library's staging-copy kernel.  By default a small kernel on the copy
                                       stream reads each run of chunks from pinned host memory (the library's

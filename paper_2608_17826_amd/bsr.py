@@ -33,7 +33,7 @@ BSR_FAIL_NONE, BSR_FAIL_MISSING, BSR_FAIL_CORRUPT = 0, 1, 2
 BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT, BSR_FAIL_BLOCK_TABLE = 3, 4, 5, 6
 
 BSR_KIND_CONTIG, BSR_KIND_PLANAR = 0, 1
-BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES, BSR_FLAG_SDMA_COPIES = 1, 2, 4
+BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES, BSR_FLAG_SDMA_COPIES, BSR_FLAG_TWO_STREAMS = 1, 2, 4, 8
 BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR, BSR_INJECT_LAUNCH_ERROR = 0, 1, 2, 3
 BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
 BSR_FILE_DIRECT = 1

@@ -65,6 +65,9 @@ uint64_t now_ns() {
 }
 
 constexpr uint64_t kAlign = 256;
+// Requests of at most this many chunk bytes are staged on the compute stream
+// (Session::one_stream).
+constexpr uint64_t kOneStreamBytes = 64ull << 20;
 constexpr uint64_t kArenaBlockAlign = 4096;
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -359,6 +362,12 @@ struct Session {  // one bound request
   uint32_t next_chunk = 0;
   bool failed = false;
   bool completing = false;  // a commit or end is waiting for its device work
+  // A small request is staged on the compute stream itself (copy == compute):
+  // stream order then does what the copy and release events do between two
+  // streams, without their hand-over latency.
+  bool one_stream = false;
+  uint32_t batch = 0;       // chunks per install launch
+  bool copy_dirty = false;  // the copy stream holds work no compute-stream wait covers yet
   int host_fail = BSR_FAIL_NONE;
   uint8_t* staging = nullptr;
   bsr_dev_status* status = nullptr;
@@ -386,7 +395,8 @@ struct bsr_ctx {
   Geometry geo;
   bsr_config cfg{};
   uint32_t W = 0;
-  uint32_t batch = 0;
+  uint32_t batch = 0;      // chunks per install launch of a request staged on the copy stream
+  uint32_t batch_one = 0;  // ... and of one staged on the compute stream
   int device = -1;
   std::mutex mu;
   Store store;
@@ -466,6 +476,7 @@ int find_active(bsr_ctx* c, uint64_t request_id, Session** out) {
 // request's ring.
 hipError_t stage_copy(bsr_ctx* c, Session& s, uint8_t* dst, const uint8_t* src, uint64_t bytes, const uint8_t* base,
                       const uint8_t* dev, uint64_t extent) {
+  s.copy_dirty = true;
   if (!c->kernel_copies || !dev || !base)
     return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s.copy);
   const bool src_in = src >= base && bytes <= extent && static_cast<uint64_t>(src - base) <= extent - bytes;
@@ -513,8 +524,11 @@ int flush_batch(bsr_ctx* c, Session& s) {
   hipEvent_t full = r.full_ev[seq % E];
   hipEvent_t freed = r.free_ev[seq % E];
   int rc;
-  if ((rc = hip_check(hipEventRecord(full, s.copy), "hipEventRecord(full)"))) return rc;
-  if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
+  if (!s.one_stream) {  // on one stream the copies already precede this install
+    if ((rc = hip_check(hipEventRecord(full, s.copy), "hipEventRecord(full)"))) return rc;
+    if ((rc = hip_check(hipStreamWaitEvent(s.compute, full, 0), "hipStreamWaitEvent(full)"))) return rc;
+    s.copy_dirty = false;
+  }
 
   // the kernel takes chunk first_chunk + c to slot first_slot + c, less W
   // once: a launch holds consecutive chunks, at most W of them
@@ -542,7 +556,7 @@ int flush_batch(bsr_ctx* c, Session& s) {
   // kernel reads only the tag partials, which the next install (later on
   // this stream) overwrites after it.  Releasing here keeps the verify off
   // the copy engine's path to the slots.
-  if ((rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
+  if (!s.one_stream && (rc = hip_check(hipEventRecord(freed, s.compute), "hipEventRecord(free)"))) return rc;
   for (uint32_t ch : chunks) s.slot_free_seq[ch % s.window] = seq;
   VerifyParams vp{};
   vp.partials = r.partials;
@@ -677,7 +691,7 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
-  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES | BSR_FLAG_SDMA_COPIES))
+  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES | BSR_FLAG_SDMA_COPIES | BSR_FLAG_TWO_STREAMS))
     return fail_with(BSR_E_ARG, "unknown config flags 0x%x", config->flags);
   // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
   // each request's ring holds its whole plan and no slot is reused.
@@ -731,6 +745,13 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
   c->kernel_copies = (config->flags & BSR_FLAG_SDMA_COPIES) == 0;
   c->W = W;
   c->batch = b;
+  // A request staged on one stream gains nothing from slack between its
+  // copies and installs (stream order serialises them): its batches take the
+  // whole window, which halves its launches at small W.  An install_batch
+  // the caller sets holds for both.
+  c->batch_one = config->install_batch ? b : std::min(W ? W : 32u, static_cast<uint32_t>(BSR_MAX_INSTALL_BATCH));
+  while (c->batch_one > b && static_cast<uint64_t>(c->batch_one) * c->geo.wg_per_chunk * bsr::kInstallThreads >= (1ull << 32))
+    --c->batch_one;
   c->device = config->hip_device;
   c->budget = B;
   c->store.index.resize(layout->n_groups);
@@ -776,8 +797,16 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
       c->xcd_log2 = bsr::xcd_log2_of(n_xcds);
     else
       (void)hipGetLastError();
-    c->partials_bytes = static_cast<uint64_t>(b) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
-    c->aux_bytes = align_up(c->partials_bytes, kAlign) + sizeof(bsr::VerifyAux);
+    auto aux_of = [&](uint32_t batch) {
+      return align_up(static_cast<uint64_t>(batch) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair), kAlign) +
+             sizeof(bsr::VerifyAux);
+    };
+    // the static array bounds one-stream batches too (never below b)
+    if (static_scratch)
+      while (c->batch_one > b && aux_of(c->batch_one) > bsr::kStaticScratchBytes) --c->batch_one;
+    const uint32_t b_max = std::max(b, c->batch_one);
+    c->partials_bytes = static_cast<uint64_t>(b_max) * c->geo.wg_per_chunk * bsr::kInstallWaves * sizeof(TagPair);
+    c->aux_bytes = aux_of(b_max);
     uint8_t* scratch = nullptr;
     if (static_scratch) {
       if (c->aux_bytes > bsr::kStaticScratchBytes) {
@@ -1289,9 +1318,17 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
     check.mode = bsr::kFinishCheckTables;
     if (int rc = hip_check(bsr::launch_finish(check, compute), "block table check launch")) return rc;
   }
+  // A request of at most kOneStreamBytes of chunks is staged on the compute
+  // stream: its copies and installs are short, and the hand-over between two
+  // streams (an event recorded on one, waited for on the other) costs about
+  // as much as they do.
+  const bool one_stream = !(c->cfg.flags & BSR_FLAG_TWO_STREAMS) &&
+                          static_cast<uint64_t>(n_hit) * c->geo.slot_bytes <= kOneStreamBytes;
   // no copy of this request may overwrite the ring before earlier compute work is done
-  if (int rc = hip_check(hipEventRecord(res.free_ev[0], compute), "hipEventRecord")) return rc;
-  if (int rc = hip_check(hipStreamWaitEvent(copy, res.free_ev[0], 0), "hipStreamWaitEvent")) return rc;
+  if (!one_stream) {
+    if (int rc = hip_check(hipEventRecord(res.free_ev[0], compute), "hipEventRecord")) return rc;
+    if (int rc = hip_check(hipStreamWaitEvent(copy, res.free_ev[0], 0), "hipStreamWaitEvent")) return rc;
+  }
 
   Session& s = c->bound[request_id];
   s = Session{};
@@ -1301,7 +1338,9 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   s.n_hit = n_hit;
   s.staging = static_cast<uint8_t*>(staging);
   s.status = status;
-  s.copy = copy;
+  s.one_stream = one_stream;
+  s.batch = one_stream ? c->batch_one : c->batch;
+  s.copy = one_stream ? compute : copy;
   s.compute = compute;
   s.ip = ip;
   s.fp = fp;
@@ -1322,7 +1361,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   st.request_id = request_id;
   st.n_hit_chunks = n_hit;
   st.window_chunks = c->W;  // 0: whole-plan mode
-  st.install_batch = c->batch;
+  st.install_batch = s.batch;
   st.slot_bytes = c->geo.slot_bytes;
   st.staging_required_bytes = need;
   st.aux_device_bytes = c->aux_bytes;
@@ -1405,7 +1444,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   auto issue_run = [&]() -> hipError_t {
     if (!run.count) return hipSuccess;
     hipError_t e = hipSuccess;
-    if (run.need >= 0 && run.need > s.copy_waited_seq) {
+    if (!s.one_stream && run.need >= 0 && run.need > s.copy_waited_seq) {
       e = hipStreamWaitEvent(s.copy, res.free_ev[run.need % E], 0);
       if (e != hipSuccess) return e;
       s.copy_waited_seq = run.need;
@@ -1509,7 +1548,8 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     }
     // the slot must have been released by the install of its previous chunk
     const uint32_t slot = i % s.window;
-    const int64_t need_seq = s.slot_free_seq[slot];
+    // on one stream stream order releases the slot: nothing to wait for
+    const int64_t need_seq = s.one_stream ? -1 : s.slot_free_seq[slot];
     uint8_t* dst = s.staging + static_cast<uint64_t>(slot) * c->geo.slot_bytes;
     hipError_t e = hipSuccess;
     if (!from_file && src_block) {
@@ -1546,6 +1586,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
       }
       if (e == hipSuccess && from_file) {
         // the bounce buffer is free again once this copy has run
+        s.copy_dirty = true;
         e = hipEventRecord(c->ftier.bounce_event(bounce), s.copy);
         ++f_used;
         if (e == hipSuccess && f_sub < fchunks.size()) {
@@ -1569,7 +1610,7 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
     batch.push_back(i);
     s.pend_tags.push_back(tg);
     ++s.st.n_chunks_enqueued;
-    if (batch.size() == c->batch)
+    if (batch.size() == s.batch)
       if ((rc = flush_all())) return rc;
   }
   if (hipError_t e = issue_run()) return fail_run(e);  // nothing of this call stays unstaged
@@ -1632,10 +1673,14 @@ static int complete_session(bsr_ctx* c, Session& s, std::unique_lock<std::mutex>
   if (!rc) rc = hip_check(hipMemcpyAsync(res.host_status, s.status, sizeof(bsr_dev_status), hipMemcpyDeviceToHost, s.compute), "status readback");
   s.completing = true;
   const hipStream_t compute = s.compute, copy = s.copy;
+  // Once the compute stream has waited for the last copy event, every copy
+  // is behind its sync; the copy stream is synchronised only if it holds
+  // work recorded after that (a run whose batch was never installed).
+  const bool sync_copy = copy != compute && s.copy_dirty;
   const uint64_t t0 = now_ns();
   lk.unlock();
   int rc2 = hip_check(hipStreamSynchronize(compute), "hipStreamSynchronize(compute)");
-  int rc3 = hip_check(hipStreamSynchronize(copy), "hipStreamSynchronize(copy)");
+  int rc3 = sync_copy ? hip_check(hipStreamSynchronize(copy), "hipStreamSynchronize(copy)") : BSR_OK;
   lk.lock();
   if (!rc) rc = rc2 ? rc2 : rc3;
   st.commit_wait_ns = now_ns() - t0;

@@ -124,6 +124,8 @@ def test_random_layout_batch_and_flags_parity(seed):
     W = int(rng.choice(w.windows))
     batch = int(rng.integers(1, min(W, bsr.BSR_MAX_INSTALL_BATCH) + 1))
     flags = bsr.BSR_FLAG_TRUSTED_TABLES if rng.random() < 0.5 else 0
+    if rng.random() < 0.5:   # these requests are small: force the two-stream path on half of them
+        flags |= bsr.BSR_FLAG_TWO_STREAMS
     say(f"case: random layout seed={seed} W={W} install_batch={batch} flags={flags}")
     case, n, _, _, res = _oracle(wi, W)
     gc = GpuCase(wi, W=W, install_batch=batch, flags=flags)
@@ -155,6 +157,8 @@ def test_config2_full_parity(batch):
 @pytest.mark.parametrize("workload,W,batch", [(1, 2, 1), (2, 32, 0)])
 @pytest.mark.parametrize("slow", ["compute", "copy"])
 def test_slot_reuse_gated_by_events_not_timing(workload, W, batch, slow):
+    """(Both workloads on two streams: the small one is forced there, since a
+    request that small is otherwise staged on the compute stream.)"""
     """Slot reuse is ordered by HIP events, not by how fast either stream
     runs.  Before every window a bounded spin kernel is queued on one of the
     session's streams: on the compute stream the installs lag far behind the
@@ -165,7 +169,7 @@ def test_slot_reuse_gated_by_events_not_timing(workload, W, batch, slow):
     say(f"case: workload {workload}, W={W}, batch={batch}, slow {slow} stream")
     wi = generate(get_config(workload))
     case, n, _, _, res = _oracle(wi, W)
-    gc = GpuCase(wi, W=W, install_batch=batch)
+    gc = GpuCase(wi, W=W, install_batch=batch, flags=bsr.BSR_FLAG_TWO_STREAMS)
     try:
         assert gc.probe(61)[0] == n
         sess = gc.session
