@@ -159,11 +159,14 @@ def main():
         torch.cuda.current_stream().synchronize()
         for r, n_k, se, d in zip(rids, ns, sessions, dsts_all):
             se.bind(r, n_k, d)
-        plans = [se.windows(n_k) for se, n_k in zip(sessions, ns)]
-        for j in range(max(len(pl) for pl in plans)):
-            for r, pl in zip(rids, plans):
-                if j < len(pl):
-                    bsr.bsr_restore_window(ctx, r, *pl[j])
+        left = list(rids)
+        while left:  # one window of each request in turn, as the library plans them
+            for r in list(left):
+                first, cnt = bsr.bsr_next_window(ctx, r)
+                if cnt == 0:
+                    left.remove(r)
+                else:
+                    bsr.bsr_restore_window(ctx, r, first, cnt)
         outs_k = [se.commit(r) for r, se in zip(rids, sessions)]
         t_c = time.perf_counter()
         for r, o, n_k in zip(rids, outs_k, ns):

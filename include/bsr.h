@@ -456,6 +456,14 @@ int bsr_request_bind(bsr_ctx* ctx, uint64_t request_id, uint32_t n_hit_chunks,
 int bsr_restore_window(bsr_ctx* ctx, uint64_t request_id, uint32_t first_chunk,
                        uint32_t n_chunks);
 
+/* The next window of the bound request's plan (§2: the confirmed prefix cut
+ * into ordered windows G_1..G_K of at most W chunks, K = ceil(n / W); in
+ * whole-plan mode one window of all n): *first_chunk and *n_chunks are what
+ * the next bsr_restore_window must pass.  *n_chunks = 0 once every window has
+ * been restored, or once the request has failed (nothing more is restored).
+ * BSR_E_STATE if the request is not bound. */
+int bsr_next_window(bsr_ctx* ctx, uint64_t request_id, uint32_t* first_chunk, uint32_t* n_chunks);
+
 /* Report group `group` of the bound request invalid outside any transfer
  * (its q_g of Eq. 6 becomes 0, e.g. the engine found an erroneous block in
  * that group).  Asynchronous, on compute_stream, after the chunks already

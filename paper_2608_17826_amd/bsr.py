@@ -125,6 +125,7 @@ def _load() -> ct.CDLL:
         "bsr_probe": (ct.c_int, [VP, U64, U64, VP, U64, P(U32), VP, VP]),
         "bsr_request_bind": (ct.c_int, [VP, U64, U32, P(bsr_group_dst), VP, U64, VP, VP, VP]),
         "bsr_restore_window": (ct.c_int, [VP, U64, U32, U32]),
+        "bsr_next_window": (ct.c_int, [VP, U64, P(U32), P(U32)]),
         "bsr_mark_group_invalid": (ct.c_int, [VP, U64, U32]),
         "bsr_commit": (ct.c_int, [VP, U64, P(U64), P(I32)]),
         "bsr_invalidate": (ct.c_int, [VP, U64, I32]),
@@ -325,6 +326,13 @@ def bsr_request_bind(ctx: Ctx, request_id: int, n_hit_chunks: int, dsts: Sequenc
 
 def bsr_restore_window(ctx: Ctx, request_id: int, first_chunk: int, n_chunks: int) -> None:
     _check(_lib.bsr_restore_window(ctx, request_id, first_chunk, n_chunks))
+
+
+def bsr_next_window(ctx: Ctx, request_id: int) -> Tuple[int, int]:
+    """(first_chunk, n_chunks) of the plan's next window; n_chunks = 0 when done."""
+    f, n = ct.c_uint32(), ct.c_uint32()
+    _check(_lib.bsr_next_window(ctx, request_id, ct.byref(f), ct.byref(n)))
+    return f.value, n.value
 
 
 def bsr_mark_group_invalid(ctx: Ctx, request_id: int, group: int) -> None:

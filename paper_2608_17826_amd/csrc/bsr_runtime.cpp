@@ -1624,6 +1624,16 @@ int bsr_restore_window(bsr_ctx* c, uint64_t request_id, uint32_t first_chunk, ui
   return BSR_OK;
 }
 
+int bsr_next_window(bsr_ctx* c, uint64_t request_id, uint32_t* first_chunk, uint32_t* n_chunks) {
+  if (!c || !first_chunk || !n_chunks) return fail_with(BSR_E_ARG, "ctx or an out-parameter is NULL");
+  std::lock_guard<std::mutex> lk(c->mu);
+  Session* s = nullptr;
+  if (int rc = find_active(c, request_id, &s)) return rc;
+  *first_chunk = s->next_chunk;
+  *n_chunks = s->failed ? 0 : std::min(s->window, s->n_hit - s->next_chunk);
+  return BSR_OK;
+}
+
 int bsr_mark_group_invalid(bsr_ctx* c, uint64_t request_id, uint32_t group) {
   if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
   if (int rc = set_device(c)) return rc;

@@ -82,8 +82,19 @@ class RestoreSession:
                        status_dict(self.status))
 
     def windows(self, n_hit: int) -> List[Tuple[int, int]]:
+        """The plan of a request not bound yet (the library's own plan, once
+        bound, comes from ``next_windows``)."""
         W = self.ctx.window_chunks or max(1, n_hit)
         return [(s, min(W, n_hit - s)) for s in range(0, n_hit, W)]
+
+    def next_windows(self, request_id: int):
+        """The bound request's remaining windows, as the library plans them:
+        each is asked for after the one before has been restored."""
+        while True:
+            first, n = bsr.bsr_next_window(self.ctx, request_id)
+            if n == 0:
+                return
+            yield first, n
 
     def restore(self, request_id: int, n_hit: int, dsts: Sequence[bsr.bsr_group_dst],
                 plan: Optional[Sequence[Tuple[int, int]]] = None, abort_after_windows: Optional[int] = None,
@@ -99,7 +110,7 @@ class RestoreSession:
         if after_bind is not None:
             after_bind()
         errors = []
-        for j, (first, n) in enumerate(plan if plan is not None else self.windows(n_hit)):
+        for j, (first, n) in enumerate(plan if plan is not None else self.next_windows(request_id)):
             try:
                 bsr.bsr_restore_window(self.ctx, request_id, first, n)
             except bsr.BsrError as e:

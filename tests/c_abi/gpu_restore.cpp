@@ -1,8 +1,9 @@
 // A torch-free restore through the C ABI: HIP runtime calls for memory and
 // streams, include/bsr.h for everything else.  Two groups with one block per
 // chunk (a contiguous group of two 1,152-byte-record tensors and a planar
-// group of 132-byte records split 128 + 4), 40 chunks stored in bulk,
-// W = 8, a reversed block table.  With block = chunk the expected pool image
+// group of 132-byte records split 128 + 4), 43 chunks stored in bulk,
+// W = 8 (five whole windows and a ragged one of 3, as bsr_next_window plans
+// them), a reversed block table.  With block = chunk the expected pool image
 // is plain concatenation, checked byte for byte here, together with the
 // exposure, the valid bytes, the staging peak and the untouched blocks.
 #include <hip/hip_runtime_api.h>
@@ -25,7 +26,7 @@
 
 namespace {
 
-constexpr uint32_t C = 64, N = 40, W = 8, POOL = N + 3;
+constexpr uint32_t C = 64, N = 43, W = 8, POOL = N + 3;
 constexpr uint32_t T0 = 2, R0 = 1152, T1 = 1, R1 = 132, S1 = 128;
 
 uint8_t byte_of(uint32_t chunk, uint32_t group, uint64_t i) {
@@ -120,8 +121,16 @@ int main() {
   HIP(hipDeviceSynchronize());
 
   CHECK(bsr_request_bind(ctx, 1, N, dst, ring, ring_bytes, status, copy, compute) == BSR_OK);
-  for (uint32_t first = 0; first < N; first += W)
-    CHECK(bsr_restore_window(ctx, 1, first, first + W <= N ? W : N - first) == BSR_OK);
+  // the windows as the library plans them: [0, W), [W, 2W), ..., a ragged last one
+  uint32_t first = 0, n = 0, n_windows = 0;
+  for (;;) {
+    CHECK(bsr_next_window(ctx, 1, &first, &n) == BSR_OK);
+    if (n == 0) break;
+    CHECK(first == n_windows * W && n == (first + W <= N ? W : N - first));
+    CHECK(bsr_restore_window(ctx, 1, first, n) == BSR_OK);
+    ++n_windows;
+  }
+  CHECK(first == N && n_windows == (N + W - 1) / W);
   uint64_t exposed = 0;
   int32_t fallback = -1;
   CHECK(bsr_commit(ctx, 1, &exposed, &fallback) == BSR_OK);

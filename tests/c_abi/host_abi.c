@@ -104,6 +104,10 @@ int main(int argc, char** argv) {
   /* protocol and device errors on a host-only context */
   CHECK(bsr_restore_window(ctx, 8, 0, 1) == BSR_E_DEVICE);
   CHECK(bsr_commit(ctx, 8, NULL, NULL) == BSR_E_DEVICE);
+  uint32_t w_first = 7, w_n = 7;
+  CHECK(bsr_next_window(ctx, 8, &w_first, &w_n) == BSR_E_STATE);  /* nothing is bound */
+  CHECK(bsr_next_window(ctx, 8, NULL, &w_n) == BSR_E_ARG);
+  CHECK(bsr_next_window(NULL, 8, &w_first, &w_n) == BSR_E_ARG);
   uint8_t tiers[N_CHUNKS];
   CHECK(bsr_plan_tiers(ctx, 8, tiers, N_CHUNKS) == BSR_OK);
   CHECK(tiers[0] == BSR_TIER_PINNED && tiers[2] == BSR_TIER_NONE);

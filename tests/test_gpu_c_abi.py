@@ -1,7 +1,7 @@
 """A torch-free restore on the GPU through the C ABI (GPU).
 
 ``tests/c_abi/gpu_restore`` (built by ``build()``) allocates with the HIP
-runtime only, stores 40 chunks in bulk, binds, restores them window by
+runtime only, stores 43 chunks in bulk, binds, restores them window by
 window (W = 8) through a reversed block table and commits; it checks the
 pool image (plain concatenation, since a block holds one chunk here; both
 planes of the planar group), the valid bytes, the exposure, the staging
@@ -22,7 +22,7 @@ EXE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c_abi", "gpu_res
 
 def test_torch_free_restore_through_the_c_abi():
     assert os.path.exists(EXE), f"{EXE} is not built: run __graft_entry__.build()"
-    say("case: C ABI consumer, 40 chunks, W=8, reversed block table")
+    say("case: C ABI consumer, 43 chunks, W=8, reversed block table")
     r = subprocess.run([EXE], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr
-    assert r.stdout.startswith("ok 40 chunks"), r.stdout
+    assert r.stdout.startswith("ok 43 chunks"), r.stdout

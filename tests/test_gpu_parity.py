@@ -176,7 +176,7 @@ def test_slot_reuse_gated_by_events_not_timing(workload, W, batch, slow):
         stream = sess.compute_stream if slow == "compute" else sess.copy_stream
         torch.cuda.synchronize()
         sess.bind(61, n, gc.dsts())
-        for first, cnt in sess.windows(n):
+        for first, cnt in sess.next_windows(61):
             with torch.cuda.stream(stream):
                 torch.cuda._sleep(4_000_000)  # a spin kernel of a fixed cycle count
             bsr.bsr_restore_window(gc.ctx, 61, first, cnt)
@@ -545,6 +545,47 @@ def test_empty_prefix_and_new_salt(W):
         for g in range(1):
             np.testing.assert_array_equal(gc.valid_host(g), wi.valid_init[g])
             np.testing.assert_array_equal(gc.pool_host(g), wi.sentinel_pool(g))
+    finally:
+        gc.close()
+
+
+@pytest.mark.parametrize("W,fault", [(0, None), (2, None), (3, None), (8, None), (3, 4)])
+def test_next_window_is_the_oracles_plan(W, fault):
+    """bsr_next_window hands out exactly the oracle's windows, each after the
+    one before is restored, then (n, 0); after a transfer error at chunk
+    `fault` it hands out nothing more, and the outcome is the oracle's."""
+    say(f"case: workload 1, W={W}, next-window plan, transfer fault at {fault}")
+    wi = generate(get_config(1))
+    kw = {"faults": {fault: oracle.FAIL_TRANSFER}} if fault is not None else {}
+    case, n, _, _, res = _oracle(wi, W, **kw)
+    gc = GpuCase(wi, W=W)
+    try:
+        assert gc.probe(9)[0] == n
+        if fault is not None:
+            bsr.bsr_debug_inject(gc.ctx, bsr.BSR_INJECT_TRANSFER_ERROR, fault, 0)
+        torch.cuda.synchronize()
+        gc.session.bind(9, n, gc.dsts())
+        got, errors = [], []
+        while True:
+            first, cnt = bsr.bsr_next_window(gc.ctx, 9)
+            if cnt == 0:
+                break
+            got.append(range(first, first + cnt))
+            try:
+                bsr.bsr_restore_window(gc.ctx, 9, first, cnt)
+            except bsr.BsrError as e:
+                errors.append((first, e.code))
+        plan = oracle.plan_windows(n, W)
+        if fault is None:
+            assert got == plan and first == n and not errors
+        else:
+            j = fault // W
+            assert got == plan[:j + 1] and len(errors) == 1 and errors[0][0] == plan[j].start
+        out = gc.session.commit(9, errors)
+        if fault is None:
+            _compare_success(gc, case, res, out)
+        else:
+            _compare_failure(gc, case, res, out)
     finally:
         gc.close()
 
