@@ -113,7 +113,8 @@ extern "C" {
                                       stream reads each run of chunks from pinned host memory (the library's
                                       arena, an adopted arena that HIP reports pinned over its whole range,
                                       or the file tier's bounce buffers) into the ring; a source HIP does not
-                                      report pinned is always copied by the copy engine */
+                                      report pinned is always copied by the copy engine, and so is every run
+                                      staged on a copy stream while more than one request is bound */
 
 /* fault injection (bsr_debug_inject), forced from the host */
 #define BSR_INJECT_NONE 0

@@ -60,8 +60,6 @@ class Tenant:
                                            wi.block_tables, self.case.pools, self.case.valid, **okw)
         self.dev = place(wi)
         self.sess = RestoreSession(ctx)
-        self.windows = self.sess.windows(self.n)
-        self.next = 0
         self.errors = []
         self.out = None
 
@@ -78,10 +76,11 @@ class Tenant:
 
     def step(self):
         """Restore the next window; False when none is left or the request failed."""
-        if self.next >= len(self.windows) or self.errors:
+        if self.errors:
             return False
-        first, n = self.windows[self.next]
-        self.next += 1
+        first, n = bsr.bsr_next_window(self.ctx, self.rid)
+        if n == 0:
+            return False
         try:
             bsr.bsr_restore_window(self.ctx, self.rid, first, n)
         except bsr.BsrError as e:
@@ -179,6 +178,8 @@ def test_two_bound_interleaved_third_waits_for_budget():
         _interleave([b, c])
         b.commit()
         c.commit()
+        # runs staged while another request was bound went to the copy engine
+        assert a.out.stats["n_stage_launches"] == b.out.stats["n_stage_launches"] == 0
         events = [("bind", 10, 32), ("bind", 11, 32), ("bind", 12, 32), ("end", 10), ("bind", 12, 32),
                   ("end", 11), ("end", 12)]
         want = adm.replay(B, st["max_bound_requests"], W, slot, events)

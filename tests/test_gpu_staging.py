@@ -48,6 +48,7 @@ def test_copy_engine_staging_parity(W, batch):
         assert gc.probe(1)[0] == n
         out = gc.restore(1, n)
         _check(wi, case, res, out, gc.dev.pools, gc.dev.valid)
+        assert out.stats["n_stage_launches"] == 0
     finally:
         gc.close()
 
@@ -98,6 +99,10 @@ def test_adopted_arena(arena):
         assert got_n == n
         out = sess.restore(3, n, group_dsts(dev.block_tables, dev.tensor_bases, dev.valid, wi.pool_blocks))
         _check(wi, case, res, out, dev.pools, dev.valid)
+        if arena == "pageable":
+            assert out.stats["n_stage_launches"] == 0
+        else:
+            assert out.stats["n_stage_launches"] > 0 and out.stats["stage_bytes"] == res.h2d_bytes
         bsr.bsr_request_end(ctx, 3)
     finally:
         bsr.bsr_ctx_destroy(ctx)
