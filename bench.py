@@ -57,9 +57,10 @@ def parse():
                     help="staging copies by the library's kernel (default) or by the copy engine")
     ap.add_argument("--two-streams", action="store_true",
                     help="stage on the copy stream whatever the request's size (BSR_FLAG_TWO_STREAMS)")
-    ap.add_argument("--only-group", type=int, default=-1,
-                    help="profiling: install one group of the workload alone, its tensor count scaled so that a "
-                         "chunk holds as many bytes as the whole layout's chunk (the same launch size)")
+    ap.add_argument("--only-group", default="",
+                    help="profiling: install these groups of the workload alone (comma-separated indices), their "
+                         "tensor counts scaled together so that a chunk holds as many bytes as the whole layout's "
+                         "chunk (the same launch size)")
     ap.add_argument("--scatter-ceiling", action="store_true",
                     help="also measure a plain scattered copy of each group's block size at the install's "
                          "launch size (bsr_measure_scatter)")
@@ -85,8 +86,8 @@ def main():
     from workloads.device import place
 
     w = get_config(args.workload)
-    if args.only_group >= 0:
-        w = group_alone(w, args.only_group)
+    if args.only_group:
+        w = groups_alone(w, [int(x) for x in args.only_group.split(",")])
     W = args.window
     log(f"[bench] workload {w.index} {w.name}: generating inputs")
     wi = generate(w)
@@ -360,18 +361,23 @@ def main():
     bsr.bsr_ctx_destroy(ctx)
 
 
-def group_alone(w, g):
-    """Workload w with only group g, its tensor count scaled so that a chunk
-    holds about as many bytes as the whole layout's chunk: install launches of
-    the same size as the layout's, built from that group's blocks alone."""
+def groups_alone(w, gs):
+    """Workload w with only the groups gs, their tensor counts scaled by one
+    factor so that a chunk holds about as many bytes as the whole layout's
+    chunk: install launches of the same size as the layout's, built from
+    those groups' blocks alone, in the same byte shares among themselves."""
     import dataclasses
 
-    spec = w.groups[g]
+    if not gs or len(set(gs)) != len(gs) or not all(0 <= g < len(w.groups) for g in gs):
+        raise SystemExit(f"--only-group: distinct group indices in 0..{len(w.groups) - 1}")
     per_token = sum(s.n_tensors * s.record_bytes for s in w.groups)
-    nt = max(1, round(per_token / spec.record_bytes))
+    sub = sum(w.groups[g].n_tensors * w.groups[g].record_bytes for g in gs)
+    specs = tuple(dataclasses.replace(w.groups[g], n_tensors=max(1, round(w.groups[g].n_tensors * per_token / sub)))
+                  for g in sorted(gs))
+    nt = max(s.n_tensors for s in specs)
     base = max(w.base_records or 0, nt * w.chunk_tokens + w.held_chunks)
-    return dataclasses.replace(w, name=f"{w.name}-{spec.name}-alone",
-                               groups=(dataclasses.replace(spec, n_tensors=nt),), base_records=base,
+    name = "+".join(s.name for s in specs)
+    return dataclasses.replace(w, name=f"{w.name}-{name}-alone", groups=specs, base_records=base,
                                failure=None, failure_group=None)
 
 

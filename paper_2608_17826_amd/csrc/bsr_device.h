@@ -158,8 +158,9 @@ struct InstallHead {
   uint32_t n_groups;
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
   // Workgroups are issued group by group (contiguous groups by descending
-  // piece size, planar groups just before the last contiguous group); within
-  // a group, chunk by chunk.  start[o] is the first work item of dispatch
+  // piece size, then block size, planar groups just before the last
+  // contiguous group); within a group, chunk by chunk, first to last, or, at
+  // odd dispatch positions when `serpentine` is 1, last to first.  start[o] is the first work item of dispatch
   // position o in this launch (n_chunks times the workgroups per chunk of
   // the positions before it); positions past the last group hold the grid
   // size, which no work item reaches.
@@ -171,7 +172,8 @@ struct InstallHead {
   TagPair* partials;        // [n_chunks * wg_per_chunk * kInstallWaves], one per wave, chunk-major
   uint32_t lds_bytes;       // dynamic LDS of this launch
   uint32_t xcd_full;        // hardware workgroups below it are remapped across the XCDs
-  uint32_t pad[6];
+  uint32_t serpentine;      // 1: odd dispatch positions take the launch's chunks last to first
+  uint32_t pad[5];
 };
 
 struct InstallGroup {

@@ -380,8 +380,9 @@ __global__ __launch_bounds__(kInstallThreads) void k_install(const InstallParams
   for (uint32_t q = 1; q < BSR_MAX_GROUPS; ++q) oi = add_if_ge(oi, bid, H.start[q]);
   const InstallGroup G = load_args(&p.g[oi]);
   uint32_t rem = bid - H.n_chunks * G.prefix;
-  const uint32_t c = packed_div(G.div_per_chunk.m, G.div_per_chunk.s, rem);
-  rem -= c * G.per_chunk;
+  const uint32_t cf = packed_div(G.div_per_chunk.m, G.div_per_chunk.s, rem);
+  rem -= cf * G.per_chunk;
+  const uint32_t c = (oi & H.serpentine) ? H.n_chunks - 1 - cf : cf;  // launch-relative chunk
   const uint32_t wg = c * H.wg_per_chunk + G.wg_start + rem;  // chunk-major slot of the tag partials
 
   const uint32_t r1 = packed_div(G.div_pieces.m, G.div_pieces.s, rem);

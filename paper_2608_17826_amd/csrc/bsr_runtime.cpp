@@ -68,6 +68,13 @@ constexpr uint64_t kAlign = 256;
 // Requests of at most this many chunk bytes are staged on the compute stream
 // (Session::one_stream).
 constexpr uint64_t kOneStreamBytes = 64ull << 20;
+// Install launches whose staged chunks exceed this many bytes walk their
+// chunks in alternate directions from one dispatch position to the next
+// (InstallHead::serpentine).  Measured on the 512K 4-group layout: launches
+// of 28 and 56 chunks (459 and 919 MB) gain 1.5-1.6 points of 8 TB/s; 14
+// chunks (230 MB) gain nothing and 7 chunks lose 0.4.  The gain starts
+// where a launch outgrows the 256 MiB Infinity Cache in front of HBM.
+constexpr uint64_t kSerpentineBytes = 256ull << 20;
 constexpr uint64_t kArenaBlockAlign = 4096;
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -236,17 +243,20 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
   G->wg_start[L->n_groups] = wg;
   for (uint32_t g = L->n_groups + 1; g <= BSR_MAX_GROUPS; ++g) G->wg_start[g] = wg;
   G->wg_per_chunk = wg;
-  // dispatch order: contiguous groups by descending piece size, with the
-  // planar (LDS-staged) groups placed just before the last contiguous group,
-  // so that planar pieces, the slowest per workgroup, never form a launch's
-  // tail.  Measured with four install workgroups per CU: 512K 4-group
-  // layout 70.2% of 8 TB/s (planar first 69.5-69.7%, planar last 69.9%);
-  // 2-group layout 71.1% (planar first, the same order there, 70.9-71.2%;
-  // planar last 70.0%)
+  // dispatch order: contiguous groups by descending piece size, then
+  // descending block size, with the planar (LDS-staged) groups placed just
+  // before the last contiguous group, so that planar pieces, the slowest per
+  // workgroup, never form a launch's tail.  On the 512K 4-group layout
+  // (three contiguous groups of 8 KiB pieces) the block-size tie-break puts
+  // the 16 KB-block group last: 76.4% -> 76.8% of 8 TB/s at W = 32, 76.2 ->
+  // 78.3% at W = 16, 62.9 -> 67.2% at W = 8 (planar last: 75.2%)
   uint32_t contig[BSR_MAX_GROUPS], planar[BSR_MAX_GROUPS], nc = 0, np = 0;
   for (uint32_t g = 0; g < L->n_groups; ++g) (G->gg[g].kind == BSR_KIND_PLANAR ? planar[np++] : contig[nc++]) = g;
-  std::stable_sort(contig, contig + nc,
-                   [&](uint32_t a, uint32_t b) { return G->gg[a].piece_bytes > G->gg[b].piece_bytes; });
+  std::stable_sort(contig, contig + nc, [&](uint32_t a, uint32_t b) {
+    const GroupGeom &x = G->gg[a], &y = G->gg[b];
+    if (x.piece_bytes != y.piece_bytes) return x.piece_bytes > y.piece_bytes;
+    return static_cast<uint64_t>(x.block_tokens) * x.record_bytes > static_cast<uint64_t>(y.block_tokens) * y.record_bytes;
+  });
   uint32_t pos = 0;
   for (uint32_t i = 0; i + 1 < nc; ++i) G->order[pos++] = contig[i];
   for (uint32_t i = 0; i < np; ++i) G->order[pos++] = planar[i];
@@ -545,6 +555,7 @@ int flush_batch(bsr_ctx* c, Session& s) {
   ip.h.first_slot = chunks.front() % s.window;
   for (uint32_t o = 0; o < BSR_MAX_GROUPS; ++o) ip.h.start[o] = ip.h.n_chunks * c->geo.order_prefix[o];
   ip.h.xcd_full = bsr::xcd_remap_bound(ip.h.n_chunks * ip.h.wg_per_chunk, ip.h.xcd_log2);
+  ip.h.serpentine = static_cast<uint64_t>(ip.h.n_chunks) * c->geo.slot_bytes > kSerpentineBytes ? 1u : 0u;
   hipEvent_t t0 = nullptr, t1 = nullptr;
   if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
