@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_side import GpuCase, say
+from gpu_side import GpuCase, layout_of, say
 from oracle_side import build_case
 from paper_2608_17826_amd import bsr
 from workloads import generate, get_config
@@ -461,6 +461,42 @@ def test_max_groups_and_max_install_batch():
         assert out.stats["install_batch"] == 32 and out.stats["n_install_launches"] == 2
     finally:
         gc.close()
+
+
+def _serpentine_workload():
+    """Five groups whose 28-chunk install launches exceed 256 MiB, so that the
+    groups at odd dispatch positions take a launch's chunks last to first:
+    three contiguous groups with equal piece sizes and different block sizes
+    (one not dividing the chunk), two planar groups, a ragged token tail."""
+    from workloads.configs import GroupSpec
+    specs = [GroupSpec("a", 64, 24, 1152, value_kind="bytes"),
+             GroupSpec("b", 128, 40, 132, kind="planar", split_bytes=128, value_kind="bytes"),
+             GroupSpec("c", 32, 8, 512, value_kind="bytes"),
+             GroupSpec("d", 96, 2, 1152, value_kind="bytes"),
+             GroupSpec("e", 64, 16, 132, kind="planar", split_bytes=128, value_kind="bytes")]
+    return Workload(index=301, name="serpentine-5g", n_tokens=40 * 256 + 100, chunk_tokens=256,
+                    groups=tuple(specs), windows=(32,), pool_factor=2, base_records=1 << 14)
+
+
+def test_serpentine_launches_full_parity():
+    """Launches of 28 (the default batch) or 32 chunks take the serpentine
+    order, the last, ragged launch (12 or 8 chunks) does not; the whole image
+    is the oracle's either way."""
+    wi = generate(_serpentine_workload())
+    slot = bsr.bsr_slot_bytes(layout_of(wi))
+    assert 28 * slot > (256 << 20) and 12 * slot <= (256 << 20)
+    case, n, _, _, res = _oracle(wi, 32)
+    assert n == 40
+    for rid, batch in ((14, 0), (15, 32)):
+        say(f"case: five groups, {slot} B chunks, W=32, install batch {batch or 28}, serpentine launches")
+        gc = GpuCase(wi, W=32, install_batch=batch)
+        try:
+            assert gc.probe(rid)[0] == n
+            out = gc.restore(rid, n)
+            _compare_success(gc, case, res, out)
+            assert out.stats["n_install_launches"] == 2
+        finally:
+            gc.close()
 
 
 def test_copy_runs_follow_the_arena_layout():
