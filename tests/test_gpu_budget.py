@@ -232,6 +232,38 @@ def test_failure_in_one_request_leaves_the_others_intact():
         bsr.bsr_ctx_destroy(ctx)
 
 
+def test_staging_path_changes_mid_request():
+    """A request staged by the staging kernel while bound alone switches to
+    the copy engine when a second one binds, and back once the second one
+    has committed; both images are the oracle's."""
+    W = 8
+    wis = [_variant(2, 2 + 100 * j, n_tokens=8192) for j in range(2)]
+    ctx, slot = _ctx(wis, W, budget=2 * W * 9_707_520)
+    try:
+        x = Tenant(ctx, wis[0], 70, W)
+        y = Tenant(ctx, wis[1], 71, W)
+        assert x.probe() == y.probe() == 32
+        say("case: config-2 layout 8K x2, W=8: x alone, then with y, then alone again")
+        log = []
+        assert _bind(x, log)
+        assert x.step() and x.step()          # windows 0-1 of x alone: staging kernel
+        assert _bind(y, log)
+        assert x.step() and y.step()          # x's window 2 beside y: copy engine
+        while y.step():
+            pass
+        y.commit()
+        while x.step():                       # x's window 3 alone again
+            pass
+        x.commit()
+        x.check_success()
+        y.check_success()
+        runs_x, runs_y = x.out.stats["n_stage_launches"], y.out.stats["n_stage_launches"]
+        assert runs_x > 0 and runs_y == 0
+        assert 0 < x.out.stats["stage_bytes"] < x.out.stats["h2d_bytes"]
+    finally:
+        bsr.bsr_ctx_destroy(ctx)
+
+
 def test_budget_zero_keeps_the_lock_and_slot_count_limits():
     W = 2
     wis = [_variant(1, 1 + 100 * j) for j in range(3)]
