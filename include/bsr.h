@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define BSR_ABI_VERSION 3
+#define BSR_ABI_VERSION 4
 #define BSR_MAX_GROUPS 8
 #define BSR_MAX_INSTALL_BATCH 32
 #define BSR_MAX_BOUND_REQUESTS 16 /* session slots of one context */
@@ -97,7 +97,11 @@ extern "C" {
 #define BSR_KIND_PLANAR 1
 
 /* bsr_config.flags */
-#define BSR_FLAG_TIME_INSTALL 1u  /* time every install and staging-copy launch with HIP events */
+#define BSR_FLAG_TIME_INSTALL 1u  /* time every install launch with HIP events */
+#define BSR_FLAG_TIME_STAGE 16u   /* time every staging-kernel launch with HIP events.  Each stamp on the
+                                      copy stream lengthens the gap between two consecutive staging copies,
+                                      which the restore then pays (0.2-0.4% of a 512K restore at W = 32,
+                                      1% at W = 8) */
 #define BSR_FLAG_TRUSTED_TABLES 2u /* bind does not read the block tables back, so it never waits for the
                                       compute stream (an engine's model work may be queued there); the
                                       tables are checked on the device after the begin kernel instead: an
@@ -233,7 +237,7 @@ typedef struct bsr_stats {
   uint32_t file_tier_chunks;       /* chunks restored from the file tier */
   uint32_t n_stage_launches;       /* staging-copy kernel launches (0 when the copy engine staged) */
   uint64_t stage_bytes;            /* bytes those launches moved from pinned host memory */
-  double stage_ms_total;           /* sum of their durations (BSR_FLAG_TIME_INSTALL) */
+  double stage_ms_total;           /* sum of their durations (BSR_FLAG_TIME_STAGE) */
 } bsr_stats;
 
 /* Admission state of a context (the lock or the global budget B). */
@@ -255,6 +259,12 @@ typedef struct bsr_ctx bsr_ctx;
 
 /* BSR_ABI_VERSION of the loaded library. */
 int32_t bsr_abi_version(void);
+
+/* Instrumentation: set the context's timing flags (BSR_FLAG_TIME_INSTALL,
+ * BSR_FLAG_TIME_STAGE; the other config flags are kept).  A request takes
+ * the flags in force when it is bound, so its counters always describe
+ * the same launches.  BSR_E_ARG for any other bit. */
+int bsr_set_timing(bsr_ctx* ctx, uint32_t flags);
 
 /* sizeof of the public struct named by a BSR_STRUCT_* id, 0 if unknown
  * (lets bindings check their struct mirrors). */

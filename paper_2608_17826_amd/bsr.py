@@ -18,7 +18,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbsr.so")
 
-BSR_ABI_VERSION = 3
+BSR_ABI_VERSION = 4
 BSR_MAX_GROUPS = 8
 BSR_MAX_INSTALL_BATCH = 32
 BSR_MAX_BOUND_REQUESTS = 16
@@ -34,6 +34,7 @@ BSR_FAIL_TIMEOUT, BSR_FAIL_TRANSFER, BSR_FAIL_ABORT, BSR_FAIL_BLOCK_TABLE = 3, 4
 
 BSR_KIND_CONTIG, BSR_KIND_PLANAR = 0, 1
 BSR_FLAG_TIME_INSTALL, BSR_FLAG_TRUSTED_TABLES, BSR_FLAG_SDMA_COPIES, BSR_FLAG_TWO_STREAMS = 1, 2, 4, 8
+BSR_FLAG_TIME_STAGE = 16
 BSR_INJECT_NONE, BSR_INJECT_DELAY_MS, BSR_INJECT_TRANSFER_ERROR, BSR_INJECT_LAUNCH_ERROR = 0, 1, 2, 3
 BSR_TIER_PINNED, BSR_TIER_FILE, BSR_TIER_NONE = 0, 1, 255
 BSR_FILE_DIRECT = 1
@@ -106,6 +107,7 @@ def _load() -> ct.CDLL:
     P, U32, U64, I32, VP = ct.POINTER, ct.c_uint32, ct.c_uint64, ct.c_int32, ct.c_void_p
     sig = {
         "bsr_abi_version": (I32, []),
+        "bsr_set_timing": (ct.c_int, [VP, U32]),
         "bsr_struct_size": (U64, [I32]),
         "bsr_last_error": (ct.c_char_p, []),
         "bsr_slot_bytes": (U64, [P(bsr_layout)]),
@@ -174,6 +176,10 @@ def _ptr(a: np.ndarray) -> int:
 # ---- library / layout -------------------------------------------------------
 def bsr_abi_version() -> int:
     return _lib.bsr_abi_version()
+
+
+def bsr_set_timing(ctx: "Ctx", flags: int) -> None:
+    _check(_lib.bsr_set_timing(ctx, flags))
 
 
 def bsr_last_error() -> str:

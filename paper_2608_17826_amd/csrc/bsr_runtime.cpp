@@ -75,6 +75,7 @@ constexpr uint64_t kOneStreamBytes = 64ull << 20;
 // chunks (230 MB) gain nothing and 7 chunks lose 0.4.  The gain starts
 // where a launch outgrows the 256 MiB Infinity Cache in front of HBM.
 constexpr uint64_t kSerpentineBytes = 256ull << 20;
+constexpr uint32_t kTimingFlags = BSR_FLAG_TIME_INSTALL | BSR_FLAG_TIME_STAGE;
 constexpr uint64_t kArenaBlockAlign = 4096;
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -378,6 +379,7 @@ struct Session {  // one bound request
   bool one_stream = false;
   uint32_t batch = 0;       // chunks per install launch
   bool copy_dirty = false;  // the copy stream holds work no compute-stream wait covers yet
+  uint32_t time_flags = 0;  // BSR_FLAG_TIME_INSTALL / BSR_FLAG_TIME_STAGE, taken at bind
   int host_fail = BSR_FAIL_NONE;
   uint8_t* staging = nullptr;
   bsr_dev_status* status = nullptr;
@@ -499,7 +501,7 @@ hipError_t stage_copy(bsr_ctx* c, Session& s, uint8_t* dst, const uint8_t* src, 
                       static_cast<uint64_t>(dst - s.staging) <= s.ring_bytes - bytes;
   if (!src_in || !dst_in) return hipErrorInvalidValue;
   hipEvent_t t0 = nullptr, t1 = nullptr;
-  if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
+  if (s.time_flags & BSR_FLAG_TIME_STAGE) {
     t0 = take_timing_event(c);
     t1 = take_timing_event(c);
     if (!t0 || !t1) {
@@ -557,10 +559,14 @@ int flush_batch(bsr_ctx* c, Session& s) {
   ip.h.xcd_full = bsr::xcd_remap_bound(ip.h.n_chunks * ip.h.wg_per_chunk, ip.h.xcd_log2);
   ip.h.serpentine = static_cast<uint64_t>(ip.h.n_chunks) * c->geo.slot_bytes > kSerpentineBytes ? 1u : 0u;
   hipEvent_t t0 = nullptr, t1 = nullptr;
-  if (c->cfg.flags & BSR_FLAG_TIME_INSTALL) {
+  if (s.time_flags & BSR_FLAG_TIME_INSTALL) {
     t0 = take_timing_event(c);
     t1 = take_timing_event(c);
-    if (!t0 || !t1) t0 = t1 = nullptr;
+    if (!t0 || !t1) {
+      if (t0) c->timing_pool.push_back(t0);
+      if (t1) c->timing_pool.push_back(t1);
+      t0 = t1 = nullptr;
+    }
   }
   if ((rc = hip_check(bsr::launch_install(ip, ip.h.n_chunks * ip.h.wg_per_chunk, s.compute, t0, t1), "install launch"))) {
     if (t0) c->timing_pool.push_back(t0);
@@ -707,7 +713,7 @@ static int ctx_create(const bsr_layout* layout, const bsr_config* config, bsr_ct
   *out = nullptr;
   if (int rc = check_layout(layout)) return rc;
   if (!config) return fail_with(BSR_E_ARG, "config is NULL");
-  if (config->flags & ~(BSR_FLAG_TIME_INSTALL | BSR_FLAG_TRUSTED_TABLES | BSR_FLAG_SDMA_COPIES | BSR_FLAG_TWO_STREAMS))
+  if (config->flags & ~(kTimingFlags | BSR_FLAG_TRUSTED_TABLES | BSR_FLAG_SDMA_COPIES | BSR_FLAG_TWO_STREAMS))
     return fail_with(BSR_E_ARG, "unknown config flags 0x%x", config->flags);
   // W = 0 is the legacy whole-plan mode (§4 "Restore-window configuration"):
   // each request's ring holds its whole plan and no slot is reused.
@@ -1355,6 +1361,7 @@ int bsr_request_bind(bsr_ctx* c, uint64_t request_id, uint32_t n_hit, const bsr_
   s.staging = static_cast<uint8_t*>(staging);
   s.status = status;
   s.one_stream = one_stream;
+  s.time_flags = c->cfg.flags & kTimingFlags;
   s.batch = one_stream ? c->batch_one : c->batch;
   s.copy = one_stream ? compute : copy;
   s.compute = compute;
@@ -1774,6 +1781,14 @@ int bsr_commit(bsr_ctx* c, uint64_t request_id, uint64_t* exposed_tokens, int32_
   Session* s = nullptr;
   if (int rc = find_active(c, request_id, &s)) return rc;
   return complete_session(c, *s, lk, true, exposed_tokens, fallback);
+}
+
+int bsr_set_timing(bsr_ctx* c, uint32_t flags) {
+  if (!c) return fail_with(BSR_E_ARG, "ctx is NULL");
+  if (flags & ~kTimingFlags) return fail_with(BSR_E_ARG, "flags 0x%x are not timing flags", flags);
+  std::lock_guard<std::mutex> lk(c->mu);
+  c->cfg.flags = (c->cfg.flags & ~kTimingFlags) | flags;
+  return BSR_OK;
 }
 
 int bsr_request_running(bsr_ctx* c, uint64_t request_id) {

@@ -104,6 +104,10 @@ int main(int argc, char** argv) {
   /* protocol and device errors on a host-only context */
   CHECK(bsr_restore_window(ctx, 8, 0, 1) == BSR_E_DEVICE);
   CHECK(bsr_commit(ctx, 8, NULL, NULL) == BSR_E_DEVICE);
+  CHECK(bsr_set_timing(ctx, BSR_FLAG_TIME_INSTALL | BSR_FLAG_TIME_STAGE) == BSR_OK);
+  CHECK(bsr_set_timing(ctx, 0) == BSR_OK);
+  CHECK(bsr_set_timing(ctx, BSR_FLAG_SDMA_COPIES) == BSR_E_ARG);  /* not a timing flag */
+  CHECK(bsr_set_timing(NULL, 0) == BSR_E_ARG);
   uint32_t w_first = 7, w_n = 7;
   CHECK(bsr_next_window(ctx, 8, &w_first, &w_n) == BSR_E_STATE);  /* nothing is bound */
   CHECK(bsr_next_window(ctx, 8, NULL, &w_n) == BSR_E_ARG);

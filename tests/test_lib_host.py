@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol():
     nm = subprocess.run(["nm", "-D", "--defined-only", bsr.LIB_PATH], capture_output=True, text=True).stdout
     exported = set(re.findall(r" T (bsr_[a-z0-9_]+)", nm))
     assert set(names) <= exported
-    assert bsr.bsr_abi_version() == bsr.BSR_ABI_VERSION == 3
+    assert bsr.bsr_abi_version() == bsr.BSR_ABI_VERSION == 4
 
 
 def _layout(w):
