@@ -159,11 +159,12 @@ struct InstallHead {
   uint32_t wg_per_chunk;    // workgroups per chunk, all groups
   // Workgroups are issued group by group (contiguous groups by descending
   // piece size, then block size, planar groups just before the last
-  // contiguous group); within a group, chunk by chunk, first to last, or, at
-  // odd dispatch positions when `serpentine` is 1, last to first.  start[o] is the first work item of dispatch
-  // position o in this launch (n_chunks times the workgroups per chunk of
-  // the positions before it); positions past the last group hold the grid
-  // size, which no work item reaches.
+  // contiguous group); within a group, chunk by chunk, first to last, or,
+  // at odd dispatch positions when `serpentine` is 1, last to first.
+  // start[o] is the first work item of dispatch position o in this launch
+  // (n_chunks times the workgroups per chunk of the positions before it);
+  // positions past the last group hold the grid size, which no work item
+  // reaches.
   uint32_t start[BSR_MAX_GROUPS];
   // words 16-31
   const uint8_t* ring;

@@ -250,7 +250,8 @@ void build_geometry(const bsr_layout* L, Geometry* G) {
   // workgroup, never form a launch's tail.  On the 512K 4-group layout
   // (three contiguous groups of 8 KiB pieces) the block-size tie-break puts
   // the 16 KB-block group last: 76.4% -> 76.8% of 8 TB/s at W = 32, 76.2 ->
-  // 78.3% at W = 16, 62.9 -> 67.2% at W = 8 (planar last: 75.2%)
+  // 78.3% at W = 16, 62.9 -> 67.2% at W = 8, before the serpentine order
+  // (kSerpentineBytes) adds its own gain; planar last, with it: 75.2%
   uint32_t contig[BSR_MAX_GROUPS], planar[BSR_MAX_GROUPS], nc = 0, np = 0;
   for (uint32_t g = 0; g < L->n_groups; ++g) (G->gg[g].kind == BSR_KIND_PLANAR ? planar[np++] : contig[nc++]) = g;
   std::stable_sort(contig, contig + nc, [&](uint32_t a, uint32_t b) {
