@@ -141,3 +141,35 @@ def test_scatter_ceiling_measurement():
             bsr.bsr_measure_scatter(ctx, 16_384, 64 << 20, 1, 1, 2)     # unknown flag
     finally:
         bsr.bsr_ctx_destroy(ctx)
+
+
+def test_timing_flags_are_taken_at_bind():
+    """BSR_FLAG_TIME_INSTALL stamps installs only, BSR_FLAG_TIME_STAGE the
+    staging launches only; bsr_set_timing changes them for requests bound
+    afterwards, never for one already bound."""
+    wi = generate(get_config(2))
+    say("case: workload 2 (32K), W=32, timing flags per request")
+    case, n, res = _oracle(wi, 32)
+    gc = GpuCase(wi, W=32, flags=bsr.BSR_FLAG_TIME_INSTALL)
+    try:
+        def restore(rid, **kw):
+            assert gc.probe(rid)[0] == n
+            out = gc.restore(rid, n, **kw)
+            _check(wi, case, res, out, gc.dev.pools, gc.dev.valid)
+            bsr.bsr_request_end(gc.ctx, rid)
+            return out.stats
+
+        st = restore(31)
+        assert st["install_ms_total"] > 0 and st["n_stage_launches"] > 0 and st["stage_ms_total"] == 0
+        bsr.bsr_set_timing(gc.ctx, bsr.BSR_FLAG_TIME_STAGE)
+        st = restore(32)
+        assert st["install_ms_total"] == 0 and st["stage_ms_total"] > 0
+        # changed while bound: this request keeps the flags of its bind
+        st = restore(33, after_bind=lambda: bsr.bsr_set_timing(gc.ctx, bsr.BSR_FLAG_TIME_INSTALL))
+        assert st["install_ms_total"] == 0 and st["stage_ms_total"] > 0
+        st = restore(34)
+        assert st["install_ms_total"] > 0 and st["stage_ms_total"] == 0
+        with pytest.raises(bsr.BsrError):
+            bsr.bsr_set_timing(gc.ctx, bsr.BSR_FLAG_SDMA_COPIES)
+    finally:
+        gc.close()
